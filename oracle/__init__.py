@@ -1,0 +1,178 @@
+"""CPU oracle for the fused weight-gradient + AdamW step (FORGE, Sec. 2.2, Algorithm 1).
+
+TEST INFRASTRUCTURE ONLY.  Only the test-suite, the smoke check and the benchmark's
+CPU-baseline leg may import this package.  It shares no code with the HIP library and
+imports nothing from it.
+
+The arithmetic lives in ``forge_oracle.c`` (plain fp64 C loops, OpenMP over rows);
+this module compiles it with gcc, loads it with ctypes and marshals numpy arrays.
+bf16 tensors are passed as ``numpy.uint16`` bit patterns.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+import threading
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "forge_oracle.c")
+_LIB = os.path.join(_HERE, "libforge_oracle.so")
+
+MOMENT_F32, MOMENT_BF16, MOMENT_I8 = 0, 1, 2
+I8_BLOCK = 256
+
+_lock = threading.Lock()
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle into ``oracle/libforge_oracle.so`` with gcc (-O3, OpenMP, no fast-math)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp"
+        subprocess.check_call(
+            ["gcc", "-O3", "-fopenmp", "-fPIC", "-shared", "-std=c11", "-Wall",
+             "-fno-fast-math", "-ffp-contract=off", _SRC, "-o", tmp, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+                build(force=True)
+            lib = ctypes.CDLL(_LIB)
+            P, I64, F32, I32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_float, ctypes.c_int
+            lib.forge_oracle_bf16_to_f64.argtypes = [ctypes.c_uint16]
+            lib.forge_oracle_bf16_to_f64.restype = ctypes.c_double
+            lib.forge_oracle_f64_to_bf16.argtypes = [ctypes.c_double]
+            lib.forge_oracle_f64_to_bf16.restype = ctypes.c_uint16
+            lib.forge_oracle_wgrad.argtypes = [P, P, I64, I64, I64, P]
+            lib.forge_oracle_wgrad.restype = None
+            lib.forge_oracle_quantize_i8.argtypes = [P, I64, I64, I32, P, P]
+            lib.forge_oracle_quantize_i8.restype = None
+            lib.forge_oracle_adamw.argtypes = [P, P, P, P, P, P, I64, I64, I32, F32, F32, F32, F32,
+                                               F32, I64, I32, P, P, P, P, P]
+            lib.forge_oracle_adamw.restype = None
+            lib.forge_oracle_num_threads.argtypes = []
+            lib.forge_oracle_num_threads.restype = I32
+            _lib = lib
+    return _lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a, dtype):
+    a = np.ascontiguousarray(a)
+    if a.dtype != dtype:
+        raise TypeError(f"expected {dtype}, got {a.dtype}")
+    return a
+
+
+def num_threads() -> int:
+    """OpenMP threads the oracle runs with (OMP_NUM_THREADS, else all host cores)."""
+    return int(_load().forge_oracle_num_threads())
+
+
+# ----------------------------------------------------------------------------- rounding
+
+def bf16_bits_to_f64(bits: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns -> exact fp64 values (bf16 is the top half of an fp32)."""
+    b = np.ascontiguousarray(bits, dtype=np.uint16)
+    return (b.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def f64_to_bf16_bits(x) -> np.ndarray:
+    """fp64 -> bf16 bit patterns, round to nearest even in one step (the oracle's C routine)."""
+    lib = _load()
+    x = np.asarray(x, dtype=np.float64)
+    out = np.empty(x.shape, dtype=np.uint16)
+    flat, of = x.reshape(-1), out.reshape(-1)
+    for i in range(flat.size):
+        of[i] = lib.forge_oracle_f64_to_bf16(float(flat[i]))
+    return out
+
+
+# ----------------------------------------------------------------------------- the method
+
+def wgrad(X: np.ndarray, dY: np.ndarray) -> np.ndarray:
+    """G = dY^T X in fp64 (Eq. wgrad): X bf16 bits [T, d_in], dY bf16 bits [T, d_out] -> [d_out, d_in]."""
+    X, dY = _c(X, np.uint16), _c(dY, np.uint16)
+    T, d_in = X.shape
+    T2, d_out = dY.shape
+    if T != T2:
+        raise ValueError("X and dY disagree on T")
+    G = np.empty((d_out, d_in), dtype=np.float64)
+    _load().forge_oracle_wgrad(_ptr(X), _ptr(dY), T, d_in, d_out, _ptr(G))
+    return G
+
+
+def quantize_i8(x: np.ndarray, second_moment: bool):
+    """Block-absmax int8 quantizer (App. B scheme, 256-row blocks along d_out).
+
+    ``x`` is fp64 [d_out, d_in]; for the second moment it holds v and sqrt(v) is stored.
+    Returns (codes int8 [d_out, d_in], scales fp32 [ceil(d_out/256), d_in]).
+    """
+    x = _c(x, np.float64)
+    d_out, d_in = x.shape
+    codes = np.empty((d_out, d_in), dtype=np.int8)
+    scales = np.empty(((d_out + I8_BLOCK - 1) // I8_BLOCK, d_in), dtype=np.float32)
+    _load().forge_oracle_quantize_i8(_ptr(x), d_in, d_out, int(second_moment), _ptr(codes), _ptr(scales))
+    return codes, scales
+
+
+def dequantize_i8(codes: np.ndarray, scales: np.ndarray, second_moment: bool) -> np.ndarray:
+    """Decode int8 moments to fp64: m = s*q, v = (s*q)^2 (the stored quantity is sqrt(v))."""
+    d_out = codes.shape[0]
+    s = np.repeat(scales.astype(np.float64), I8_BLOCK, axis=0)[:d_out]
+    x = s * codes.astype(np.float64)
+    return x * x if second_moment else x
+
+
+def adamw(G, W, m, v, *, moment_dtype, lr, beta1, beta2, eps, weight_decay, step,
+          m_scale=None, v_scale=None, round_grad_to_bf16=False, want_quotients=False):
+    """One AdamW step (Algorithm 1) on an fp64 gradient; inputs are not modified.
+
+    W: bf16 bits [d_out, d_in].  m, v: float32 / bf16 bits / int8 codes per ``moment_dtype``.
+    Returns a dict with the rounded new state (W, m, v, m_scale, v_scale) and the unrounded
+    fp64 values W64, m64, v64 (and the int8 quotients qm, qv when asked).
+    """
+    G = _c(G, np.float64)
+    d_out, d_in = G.shape
+    W = _c(W, np.uint16).copy()
+    mdt = {MOMENT_F32: np.float32, MOMENT_BF16: np.uint16, MOMENT_I8: np.int8}[moment_dtype]
+    m, v = _c(m, mdt).copy(), _c(v, mdt).copy()
+    for a in (W, m, v):
+        if a.shape != (d_out, d_in):
+            raise ValueError("state shape mismatch")
+    if moment_dtype == MOMENT_I8:
+        m_scale = _c(m_scale, np.float32).copy()
+        v_scale = _c(v_scale, np.float32).copy()
+    else:
+        m_scale = v_scale = None
+    W64, m64, v64 = (np.empty((d_out, d_in), dtype=np.float64) for _ in range(3))
+    qm = qv = None
+    if want_quotients and moment_dtype == MOMENT_I8:
+        qm, qv = np.empty((d_out, d_in), np.float64), np.empty((d_out, d_in), np.float64)
+    _load().forge_oracle_adamw(
+        _ptr(G), _ptr(W), _ptr(m), _ptr(v), _ptr(m_scale), _ptr(v_scale), d_in, d_out,
+        int(moment_dtype), float(lr), float(beta1), float(beta2), float(eps), float(weight_decay),
+        int(step), int(bool(round_grad_to_bf16)), _ptr(W64), _ptr(m64), _ptr(v64), _ptr(qm), _ptr(qv))
+    out = dict(W=W, m=m, v=v, m_scale=m_scale, v_scale=v_scale, W64=W64, m64=m64, v64=v64)
+    if qm is not None:
+        out.update(qm=qm, qv=qv)
+    return out
+
+
+def linear_step(X, dY, W, m, v, **kw):
+    """The whole fused step by definition: G = dY^T X (fp64), then ``adamw``. Also returns G."""
+    G = wgrad(X, dY)
+    out = adamw(G, W, m, v, **kw)
+    out["G"] = G
+    return out

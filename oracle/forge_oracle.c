@@ -1,0 +1,296 @@
+/*
+ * forge_oracle.c -- plain, slow, obviously-correct CPU reference for one fused
+ * weight-gradient + AdamW step of a linear layer (FORGE, Sec. 2.2, Algorithm 1).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may link, load or call
+ * this file; only the test-suite, the smoke check and the CPU-baseline leg of the
+ * benchmark do.  It shares no code, header, table or constant with the HIP
+ * library: it is written from the paper's definitions alone.
+ *
+ * What it computes (all floating point in fp64 unless stated):
+ *   1. G = dY^T X, G[p][q] = sum_{t=0}^{T-1} dY[t][p] * X[t][q], summed in token
+ *      order t = 0..T-1 (Eq. wgrad; App. A "Setup").  bf16 x bf16 products are
+ *      exact in fp64.
+ *   2. Decode the stored moments (fp32 / bf16 as they are; int8 as scale * code,
+ *      with the second moment stored through its square root).
+ *   3. AdamW exactly as Algorithm 1 states it: the two moment recurrences, the
+ *      bias corrections 1 - beta^t, and the decoupled weight update
+ *      W' = (1 - lr*wd) W - lr * mhat / (sqrt(vhat) + eps).
+ *   4. Round to the storage dtypes with round-to-nearest-even: W' to bf16 straight
+ *      from fp64; m', v' to fp32 or bf16 straight from fp64.
+ *   5. int8 moments (block-absmax scheme of App. B, with 256-row blocks along
+ *      d_out and sqrt(v) storage): per block and column, a = max |x|, scale
+ *      s = a/127, code = clamp(round_half_even(x/s)).  The paper keeps this
+ *      arithmetic in fp32, so the code decision is taken in fp32 here: x is
+ *      rounded to fp32, s is an fp32 division, x/s is an fp32 division.  The
+ *      second-moment codes are floored at 1 inside non-zero blocks (App. B: v is
+ *      kept away from zero).  The weight update reads the unquantized fp64 m', v'.
+ *
+ * Hyper-parameters arrive as the fp32 values the GPU receives; they are promoted
+ * to fp64 here, so lr = 1e-3 means (double)(float)1e-3.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORACLE_I8_BLOCK 256
+
+enum { ORACLE_MOMENT_F32 = 0, ORACLE_MOMENT_BF16 = 1, ORACLE_MOMENT_I8 = 2 };
+
+/* ---------------------------------------------------------------- bf16 helpers */
+
+/* bf16 bit pattern -> exact fp64 value (bf16 is the top half of an fp32). */
+double forge_oracle_bf16_to_f64(uint16_t h)
+{
+    uint32_t u = (uint32_t)h << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+/*
+ * fp64 -> bf16 with round-to-nearest, ties to even, in one rounding step.
+ * bf16 carries 8 significant bits; its subnormal spacing is 2^-133.  The value is
+ * scaled by a power of two so that one unit in the last place becomes 1, rounded
+ * to an integer with rint (ties-to-even under the default rounding mode) and
+ * scaled back.  Overflow past the largest bf16 gives infinity.
+ */
+uint16_t forge_oracle_f64_to_bf16(double x)
+{
+    if (isnan(x)) return (uint16_t)0x7FC0;
+    uint16_t sign = signbit(x) ? (uint16_t)0x8000 : (uint16_t)0;
+    double ax = fabs(x);
+    if (ax == 0.0) return sign;
+    if (isinf(ax)) return (uint16_t)(sign | 0x7F80);
+    int e;
+    (void)frexp(ax, &e);            /* ax = f * 2^e, 0.5 <= f < 1 */
+    int ulp_exp = e - 8;            /* 8 significant bits */
+    if (ulp_exp < -133) ulp_exp = -133;
+    double n = rint(ldexp(ax, -ulp_exp));
+    double r = ldexp(n, ulp_exp);   /* exactly representable in bf16, or 2^128 */
+    float rf = (float)r;            /* exact, or +inf on overflow */
+    uint32_t u;
+    memcpy(&u, &rf, sizeof u);
+    return (uint16_t)(sign | (uint16_t)(u >> 16));
+}
+
+/* ------------------------------------------------------------- 1. weight gradient */
+
+/*
+ * G[p*d_in + q] = sum_t dY[t*d_out + p] * X[t*d_in + q]   (Eq. wgrad, App. A)
+ * X: bf16 [T, d_in], dY: bf16 [T, d_out], both row-major.  G: fp64 [d_out, d_in].
+ * For every element the sum runs over t = 0..T-1 in order.
+ */
+void forge_oracle_wgrad(const uint16_t *X, const uint16_t *dY, int64_t T,
+                        int64_t d_in, int64_t d_out, double *G)
+{
+    double *Xd = (double *)malloc(sizeof(double) * (size_t)(T * d_in > 0 ? T * d_in : 1));
+    for (int64_t i = 0; i < T * d_in; ++i) Xd[i] = forge_oracle_bf16_to_f64(X[i]);
+
+#pragma omp parallel for schedule(dynamic, 4)
+    for (int64_t p = 0; p < d_out; ++p) {
+        double *row = G + p * d_in;
+        for (int64_t q = 0; q < d_in; ++q) row[q] = 0.0;
+        for (int64_t t = 0; t < T; ++t) {
+            double a = forge_oracle_bf16_to_f64(dY[t * d_out + p]);
+            const double *xr = Xd + t * d_in;
+            for (int64_t q = 0; q < d_in; ++q) row[q] += a * xr[q];
+        }
+    }
+    free(Xd);
+}
+
+/* ------------------------------------------------------------- int8 quantizer */
+
+/*
+ * Quantize one block column: n values x[i*stride] (fp64) -> codes, returning the
+ * fp32 scale.  floor_one: second-moment codes are clamped to [1, 127] when the
+ * block is non-zero.  quot (optional): the fp32 quotient x/s before rounding,
+ * which tests use to recognise rounding ties.
+ */
+static float quantize_column(const double *x, int64_t n, int64_t stride, int floor_one,
+                             int8_t *codes, int64_t code_stride, double *quot)
+{
+    float a = 0.0f;
+    for (int64_t i = 0; i < n; ++i) {
+        float xi = fabsf((float)x[i * stride]);
+        if (xi > a) a = xi;
+    }
+    float s = a / 127.0f;  /* fp32 division, correctly rounded */
+    for (int64_t i = 0; i < n; ++i) {
+        int code = 0;
+        float qf = 0.0f;
+        if (s > 0.0f) {
+            qf = (float)x[i * stride] / s;   /* fp32 division */
+            float r = rintf(qf);             /* ties to even */
+            if (r > 127.0f) r = 127.0f;
+            if (r < -127.0f) r = -127.0f;
+            if (floor_one && r < 1.0f) r = 1.0f;
+            code = (int)r;
+        }
+        codes[i * code_stride] = (int8_t)code;
+        if (quot) quot[i * code_stride] = (double)qf;
+    }
+    return s;
+}
+
+/*
+ * Quantize a full [d_out, d_in] fp64 matrix into int8 codes + fp32 scales
+ * [ceil(d_out/256), d_in]; the last block may hold fewer than 256 rows.
+ * is_second_moment: x holds v itself; the stored quantity is sqrt(v) with the
+ * floor-at-one rule.
+ */
+void forge_oracle_quantize_i8(const double *x, int64_t d_in, int64_t d_out,
+                              int is_second_moment, int8_t *codes, float *scales)
+{
+    int64_t nblk = (d_out + ORACLE_I8_BLOCK - 1) / ORACLE_I8_BLOCK;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t b = 0; b < nblk; ++b) {
+        int64_t r0 = b * ORACLE_I8_BLOCK;
+        int64_t n = d_out - r0 < ORACLE_I8_BLOCK ? d_out - r0 : ORACLE_I8_BLOCK;
+        double *col = (double *)malloc(sizeof(double) * (size_t)n);
+        for (int64_t q = 0; q < d_in; ++q) {
+            for (int64_t i = 0; i < n; ++i) {
+                double xv = x[(r0 + i) * d_in + q];
+                col[i] = is_second_moment ? sqrt(xv) : xv;
+            }
+            scales[b * d_in + q] = quantize_column(col, n, 1, is_second_moment,
+                                                   codes + r0 * d_in + q, d_in, NULL);
+        }
+        free(col);
+    }
+}
+
+/* ------------------------------------------------------------- 2-5. AdamW step */
+
+/*
+ * One AdamW step (Algorithm 1, state update then weight update) on a given fp64
+ * gradient G [d_out, d_in].
+ *
+ * W        bf16 [d_out, d_in], updated in place (RNE from fp64).
+ * m, v     moments in place: float* (F32), uint16_t* bf16 bits (BF16), or int8
+ *          codes (I8) with m_scale / v_scale fp32 [ceil(d_out/256), d_in].
+ * round_grad_to_bf16  round G to bf16 (RNE) before use: the gradient a two-kernel
+ *          path would have stored in a bf16 buffer (App. B, truncation bias).
+ * W64, m64, v64   optional fp64 outputs of the unrounded new values.
+ * qm, qv   optional (I8 only): the fp32 quotients x/s the codes were rounded from.
+ */
+void forge_oracle_adamw(const double *G, uint16_t *W, void *m, void *v,
+                        float *m_scale, float *v_scale, int64_t d_in, int64_t d_out,
+                        int moment_dtype, float lr, float beta1, float beta2, float eps,
+                        float weight_decay, int64_t step, int round_grad_to_bf16,
+                        double *W64, double *m64, double *v64, double *qm, double *qv)
+{
+    const double b1 = (double)beta1, b2 = (double)beta2;
+    const double eta = (double)lr, lam = (double)weight_decay, ep = (double)eps;
+    const double bc1 = 1.0 - pow(b1, (double)step);
+    const double bc2 = 1.0 - pow(b2, (double)step);
+    const double wdf = 1.0 - eta * lam;
+    const int64_t nblk = (d_out + ORACLE_I8_BLOCK - 1) / ORACLE_I8_BLOCK;
+
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t b = 0; b < nblk; ++b) {
+        int64_t r0 = b * ORACLE_I8_BLOCK;
+        int64_t n = d_out - r0 < ORACLE_I8_BLOCK ? d_out - r0 : ORACLE_I8_BLOCK;
+        double *mnew = NULL, *vroot = NULL;
+        if (moment_dtype == ORACLE_MOMENT_I8) {
+            mnew = (double *)malloc(sizeof(double) * (size_t)(n * d_in));
+            vroot = (double *)malloc(sizeof(double) * (size_t)(n * d_in));
+        }
+        for (int64_t i = 0; i < n; ++i) {
+            int64_t p = r0 + i;
+            for (int64_t q = 0; q < d_in; ++q) {
+                int64_t k = p * d_in + q;
+                double g = G[k];
+                if (round_grad_to_bf16) g = forge_oracle_bf16_to_f64(forge_oracle_f64_to_bf16(g));
+
+                double m0, v0;
+                switch (moment_dtype) {
+                case ORACLE_MOMENT_F32:
+                    m0 = (double)((const float *)m)[k];
+                    v0 = (double)((const float *)v)[k];
+                    break;
+                case ORACLE_MOMENT_BF16:
+                    m0 = forge_oracle_bf16_to_f64(((const uint16_t *)m)[k]);
+                    v0 = forge_oracle_bf16_to_f64(((const uint16_t *)v)[k]);
+                    break;
+                default: {
+                    double sm = (double)m_scale[b * d_in + q];
+                    double sv = (double)v_scale[b * d_in + q];
+                    double root = sv * (double)((const int8_t *)v)[k];
+                    m0 = sm * (double)((const int8_t *)m)[k];
+                    v0 = root * root;
+                    break;
+                }
+                }
+
+                /* Algorithm 1: state update A ... */
+                double m1 = b1 * m0 + (1.0 - b1) * g;
+                double v1 = b2 * v0 + (1.0 - b2) * g * g;
+                /* ... then weight update U, reading the new state. */
+                double mhat = m1 / bc1;
+                double vhat = v1 / bc2;
+                double w0 = forge_oracle_bf16_to_f64(W[k]);
+                double w1 = wdf * w0 - eta * mhat / (sqrt(vhat) + ep);
+
+                W[k] = forge_oracle_f64_to_bf16(w1);
+                if (W64) W64[k] = w1;
+                if (m64) m64[k] = m1;
+                if (v64) v64[k] = v1;
+                switch (moment_dtype) {
+                case ORACLE_MOMENT_F32:
+                    ((float *)m)[k] = (float)m1;
+                    ((float *)v)[k] = (float)v1;
+                    break;
+                case ORACLE_MOMENT_BF16:
+                    ((uint16_t *)m)[k] = forge_oracle_f64_to_bf16(m1);
+                    ((uint16_t *)v)[k] = forge_oracle_f64_to_bf16(v1);
+                    break;
+                default:
+                    mnew[i * d_in + q] = m1;
+                    vroot[i * d_in + q] = sqrt(v1);
+                    break;
+                }
+            }
+        }
+        if (moment_dtype == ORACLE_MOMENT_I8) {
+            int8_t *mc = (int8_t *)m, *vc = (int8_t *)v;
+            for (int64_t q = 0; q < d_in; ++q) {
+                m_scale[b * d_in + q] = quantize_column(
+                    mnew + q, n, d_in, 0, mc + r0 * d_in + q, d_in, qm ? qm + r0 * d_in + q : NULL);
+                v_scale[b * d_in + q] = quantize_column(
+                    vroot + q, n, d_in, 1, vc + r0 * d_in + q, d_in, qv ? qv + r0 * d_in + q : NULL);
+            }
+            free(mnew);
+            free(vroot);
+        }
+    }
+}
+
+/* ------------------------------------------------------- the whole fused step */
+
+/* G = dY^T X, then the AdamW step; G is returned in G_out when it is non-NULL. */
+void forge_oracle_linear_step(const uint16_t *X, const uint16_t *dY, uint16_t *W, void *m,
+                              void *v, float *m_scale, float *v_scale, int64_t T,
+                              int64_t d_in, int64_t d_out, int moment_dtype, float lr,
+                              float beta1, float beta2, float eps, float weight_decay,
+                              int64_t step, int round_grad_to_bf16, double *G_out,
+                              double *W64, double *m64, double *v64, double *qm, double *qv)
+{
+    double *G = G_out ? G_out : (double *)malloc(sizeof(double) * (size_t)(d_in * d_out > 0 ? d_in * d_out : 1));
+    forge_oracle_wgrad(X, dY, T, d_in, d_out, G);
+    forge_oracle_adamw(G, W, m, v, m_scale, v_scale, d_in, d_out, moment_dtype, lr, beta1,
+                       beta2, eps, weight_decay, step, round_grad_to_bf16, W64, m64, v64, qm, qv);
+    if (!G_out) free(G);
+}
+
+int forge_oracle_num_threads(void)
+{
+#ifdef _OPENMP
+    extern int omp_get_max_threads(void);
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

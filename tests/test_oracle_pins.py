@@ -1,0 +1,359 @@
+"""Pins for the CPU oracle: each checks it against something other than itself.
+
+Kinds of pin used here (a plausible mistake in the oracle -- a dropped term, a wrong
+sign, a transposed operand, a wrong bias correction -- fails at least one):
+
+* exact rational brute force of G = dY^T X on tiny non-square shapes;
+* the rank-one closed form of G;
+* Prop. 1 (App. A): summing the oracle's G over any partition of the token axis gives G;
+* closed forms of Algorithm 1's update (step 1 from zero state; zero gradient; beta = 0;
+  lr = 0);
+* torch.optim.AdamW in fp64 as an independent library implementation of the update;
+* bf16 round-to-nearest-even against torch's fp32 -> bf16 cast and against brute force;
+* the int8 block-absmax quantizer's invariants and App. B's accumulated-error bound.
+"""
+from fractions import Fraction
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import MOMENT_BF16, MOMENT_F32, MOMENT_I8
+
+HP = dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.1)
+
+
+def f32(x):
+    """The fp64 value of an fp32 hyper-parameter, as the oracle promotes it."""
+    return float(np.float32(x))
+
+
+def bf16_rand(shape, std, seed):
+    g = torch.Generator().manual_seed(seed)
+    t = (torch.randn(shape, generator=g) * std).to(torch.bfloat16)
+    return t.view(torch.int16).numpy().view(np.uint16).copy()
+
+
+def to_bits(values):
+    """Exact small values -> bf16 bit patterns (asserts exactness)."""
+    t = torch.tensor(values, dtype=torch.float64)
+    b = t.to(torch.float32).to(torch.bfloat16)
+    assert torch.equal(b.to(torch.float64), t), "value not exactly representable in bf16"
+    return b.view(torch.int16).numpy().view(np.uint16).copy()
+
+
+# ------------------------------------------------------------------------- bf16 rounding
+
+def test_bf16_rne_matches_torch_on_fp32_values():
+    rng = np.random.default_rng(0)
+    x = np.concatenate([
+        rng.standard_normal(20000).astype(np.float32) * np.float32(10.0) ** rng.integers(-30, 30, 20000).astype(np.float32),
+        # exact ties between neighbouring bf16 values: low 16 bits == 0x8000
+        (rng.integers(0x00800000, 0x7F000000, 2000, dtype=np.uint32) & 0xFFFF0000 | 0x8000).view(np.float32),
+        np.array([0x3F808000, 0x3F818000, 0xBF808000, 0x00008000, 0x7F7F8000], dtype=np.uint32).view(np.float32),
+    ]).astype(np.float32)
+    x = x[np.isfinite(x)]
+    want = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    got = oracle.f64_to_bf16_bits(x.astype(np.float64))
+    assert np.array_equal(got, want)
+    # hand-made ties round to even
+    assert oracle.f64_to_bf16_bits(np.array([1.0 + 2 ** -8]))[0] == 0x3F80
+    assert oracle.f64_to_bf16_bits(np.array([1.0 + 3 * 2 ** -8]))[0] == 0x3F82
+
+
+def test_bf16_rne_is_nearest_on_doubles():
+    """Direct fp64 -> bf16: brute force over the two neighbouring bf16 values."""
+    rng = np.random.default_rng(1)
+    x = rng.standard_normal(3000) * 10.0 ** rng.integers(-20, 20, 3000)
+    got = oracle.f64_to_bf16_bits(x)
+    for xi, hi in zip(x, got):
+        r = oracle.bf16_bits_to_f64(np.array([hi]))[0]
+        # neighbours of r in bf16 (same sign): r +- one ulp
+        up = oracle.bf16_bits_to_f64(np.array([hi + 1]))[0]
+        dn = oracle.bf16_bits_to_f64(np.array([hi - 1]))[0]
+        err = abs(xi - r)
+        assert err <= abs(xi - up) and err <= abs(xi - dn)
+        if err == abs(xi - up) or err == abs(xi - dn):      # a tie: result must be even
+            assert hi % 2 == 0
+
+
+# ------------------------------------------------------------------------- weight gradient
+
+def test_wgrad_exact_rationals_nonsquare():
+    T, d_in, d_out = 7, 5, 3
+    X = bf16_rand((T, d_in), 1.0, 11)
+    dY = bf16_rand((T, d_out), 0.01, 12)
+    G = oracle.wgrad(X, dY)
+    assert G.shape == (d_out, d_in)
+    Xf = oracle.bf16_bits_to_f64(X)
+    Yf = oracle.bf16_bits_to_f64(dY)
+    for p in range(d_out):
+        for q in range(d_in):
+            exact = sum(Fraction(Yf[t, p]) * Fraction(Xf[t, q]) for t in range(T))
+            bound = T * 2.0 ** -53 * sum(abs(Yf[t, p] * Xf[t, q]) for t in range(T))
+            assert abs(G[p, q] - float(exact)) <= bound
+
+
+def test_wgrad_integer_values_exact():
+    """Small integers: every partial sum is exact in fp64, so G must equal the rational sum."""
+    rng = np.random.default_rng(2)
+    T, d_in, d_out = 9, 6, 4
+    Xv = rng.integers(-8, 9, (T, d_in))
+    Yv = rng.integers(-8, 9, (T, d_out))
+    G = oracle.wgrad(to_bits(Xv.tolist()), to_bits(Yv.tolist()))
+    want = Yv.T @ Xv                                   # [d_out, d_in], integer matmul
+    assert np.array_equal(G, want.astype(np.float64))
+
+
+def test_wgrad_rank_one_closed_form():
+    """X[t,q] = a_t b_q, dY[t,p] = c_t d_p  =>  G[p,q] = (sum_t c_t a_t) d_p b_q."""
+    a = np.array([1, -2, 0.5, 3, -1.5, 0.25])
+    b = np.array([2, -1, 0.5, 4])
+    c = np.array([0.5, 1, -1, 2, 0.75, -4])
+    d = np.array([-1, 2, 0.25])
+    G = oracle.wgrad(to_bits(np.outer(a, b).tolist()), to_bits(np.outer(c, d).tolist()))
+    want = np.dot(c, a) * np.outer(d, b)
+    assert np.array_equal(G, want)
+
+
+@pytest.mark.parametrize("chunk", [1, 7, 64, 200])
+def test_wgrad_token_partition_invariance(chunk):
+    """Prop. 1: accumulating over any partition of the token axis gives G (fp64 rounding aside)."""
+    T, d_in, d_out = 200, 24, 16
+    X = bf16_rand((T, d_in), 1.0, 21)
+    dY = bf16_rand((T, d_out), 0.01, 22)
+    G = oracle.wgrad(X, dY)
+    acc = np.zeros_like(G)
+    for t0 in range(0, T, chunk):
+        acc += oracle.wgrad(X[t0:t0 + chunk], dY[t0:t0 + chunk])
+    # bound on fp64 rounding: |dY|^T |X| (a numpy product, used only as an error scale)
+    scale = np.abs(oracle.bf16_bits_to_f64(dY)).T @ np.abs(oracle.bf16_bits_to_f64(X))
+    assert np.all(np.abs(acc - G) <= 4 * T * 2.0 ** -53 * scale)
+
+
+def test_wgrad_empty_token_axis():
+    G = oracle.wgrad(np.zeros((0, 8), np.uint16), np.zeros((0, 3), np.uint16))
+    assert G.shape == (3, 8) and not G.any()
+
+
+# ------------------------------------------------------------------------- AdamW update
+
+def _state(d_out, d_in, dtype, seed, warm):
+    if not warm:
+        z = np.zeros((d_out, d_in), np.float32 if dtype == MOMENT_F32 else np.uint16)
+        return z, z.copy()
+    g = torch.Generator().manual_seed(seed)
+    m = torch.randn((d_out, d_in), generator=g) * 1e-4
+    v = (torch.randn((d_out, d_in), generator=g) * 1e-6).abs()
+    if dtype == MOMENT_F32:
+        return m.numpy().copy(), v.numpy().copy()
+    return (m.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16).copy(),
+            v.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16).copy())
+
+
+def _decode(a, dtype):
+    return a.astype(np.float64) if dtype == MOMENT_F32 else oracle.bf16_bits_to_f64(a)
+
+
+@pytest.mark.parametrize("dtype", [MOMENT_F32, MOMENT_BF16])
+def test_step1_from_zero_state_closed_form(dtype):
+    """t=1, m=v=0: m'=(1-b1)g, v'=(1-b2)g^2, mhat=g, vhat=g^2, W'=(1-lr*wd)W - lr*g/(|g|+eps)."""
+    rng = np.random.default_rng(3)
+    G = rng.standard_normal((16, 40)) * 0.1
+    W = bf16_rand((16, 40), 0.02, 31)
+    m, v = _state(16, 40, dtype, 0, warm=False)
+    out = oracle.adamw(G, W, m, v, moment_dtype=dtype, step=1, **HP)
+    b1, b2, lr, wd, eps = f32(0.9), f32(0.999), f32(1e-3), f32(0.1), f32(1e-8)
+    W0 = oracle.bf16_bits_to_f64(W)
+    np.testing.assert_allclose(out["m64"], (1 - b1) * G, rtol=1e-15, atol=0)
+    np.testing.assert_allclose(out["v64"], (1 - b2) * G * G, rtol=1e-15, atol=0)
+    np.testing.assert_allclose(out["W64"], (1 - lr * wd) * W0 - lr * G / (np.abs(G) + eps),
+                               rtol=1e-14, atol=1e-18)
+    # the update is ~ -lr*sign(g): W moves opposite to the gradient
+    assert np.all(np.sign((1 - lr * wd) * W0 - out["W64"]) == np.sign(G))
+    assert np.array_equal(out["W"], oracle.f64_to_bf16_bits(out["W64"]))
+
+
+def test_zero_gradient_cold_state_is_pure_decay():
+    W = bf16_rand((8, 24), 0.02, 41)
+    z = np.zeros((8, 24), np.float32)
+    hp = dict(HP, lr=0.5, weight_decay=0.1)            # lr*wd = 0.05: visible after bf16 rounding
+    out = oracle.adamw(np.zeros((8, 24)), W, z, z, moment_dtype=MOMENT_F32, step=7, **hp)
+    W0 = oracle.bf16_bits_to_f64(W)
+    assert np.array_equal(out["W64"], (1 - f32(0.5) * f32(0.1)) * W0)
+    assert not out["m64"].any() and not out["v64"].any()
+    assert np.array_equal(out["W"], oracle.f64_to_bf16_bits((1 - f32(0.5) * f32(0.1)) * W0))
+    assert not np.array_equal(out["W"], W)
+
+
+def test_zero_gradient_warm_state_closed_form():
+    W = bf16_rand((8, 24), 0.02, 42)
+    m, v = _state(8, 24, MOMENT_F32, 5, warm=True)
+    t = 100
+    out = oracle.adamw(np.zeros((8, 24)), W, m, v, moment_dtype=MOMENT_F32, step=t, **HP)
+    b1, b2 = f32(0.9), f32(0.999)
+    m0, v0 = m.astype(np.float64), v.astype(np.float64)
+    np.testing.assert_allclose(out["m64"], b1 * m0, rtol=1e-15)
+    np.testing.assert_allclose(out["v64"], b2 * v0, rtol=1e-15)
+    want = ((1 - f32(1e-3) * f32(0.1)) * oracle.bf16_bits_to_f64(W)
+            - f32(1e-3) * (b1 * m0 / (1 - b1 ** t)) / (np.sqrt(b2 * v0 / (1 - b2 ** t)) + f32(1e-8)))
+    np.testing.assert_allclose(out["W64"], want, rtol=1e-13, atol=1e-18)
+
+
+def test_beta_zero_is_normalised_gradient_step():
+    """b1 = b2 = 0: mhat = G, vhat = G^2 at every step, whatever the state."""
+    rng = np.random.default_rng(4)
+    G = rng.standard_normal((8, 16)) * 1e-2
+    W = bf16_rand((8, 16), 0.02, 43)
+    m, v = _state(8, 16, MOMENT_F32, 6, warm=True)
+    out = oracle.adamw(G, W, m, v, moment_dtype=MOMENT_F32, step=13,
+                       **dict(HP, beta1=0.0, beta2=0.0))
+    W0 = oracle.bf16_bits_to_f64(W)
+    want = (1 - f32(1e-3) * f32(0.1)) * W0 - f32(1e-3) * G / (np.abs(G) + f32(1e-8))
+    np.testing.assert_allclose(out["W64"], want, rtol=1e-14, atol=1e-18)
+    np.testing.assert_allclose(out["m64"], G, rtol=1e-15)
+
+
+def test_lr_zero_leaves_weight_unchanged():
+    rng = np.random.default_rng(5)
+    G = rng.standard_normal((8, 16))
+    W = bf16_rand((8, 16), 0.02, 44)
+    m, v = _state(8, 16, MOMENT_BF16, 7, warm=True)
+    out = oracle.adamw(G, W, m, v, moment_dtype=MOMENT_BF16, step=3, **dict(HP, lr=0.0))
+    assert np.array_equal(out["W"], W)
+    assert not np.array_equal(out["m"], m)
+
+
+@pytest.mark.parametrize("step", [1, 2, 100, 5000])
+def test_matches_torch_adamw_fp64(step):
+    """torch.optim.AdamW (foreach=False, fp64) is an independent implementation of the update."""
+    rng = np.random.default_rng(step)
+    d_out, d_in = 12, 20
+    G = rng.standard_normal((d_out, d_in)) * 0.02
+    W = bf16_rand((d_out, d_in), 0.02, 50 + step)
+    m, v = _state(d_out, d_in, MOMENT_F32, 8, warm=True)
+    out = oracle.adamw(G, W, m, v, moment_dtype=MOMENT_F32, step=step, **HP)
+
+    p = torch.nn.Parameter(torch.from_numpy(oracle.bf16_bits_to_f64(W)))
+    opt = torch.optim.AdamW([p], lr=f32(1e-3), betas=(f32(0.9), f32(0.999)), eps=f32(1e-8),
+                            weight_decay=f32(0.1), foreach=False, fused=False)
+    p.grad = torch.from_numpy(G.copy())
+    st = opt.state[p]
+    st["step"] = torch.tensor(float(step - 1), dtype=torch.float64)
+    st["exp_avg"] = torch.from_numpy(m.astype(np.float64))
+    st["exp_avg_sq"] = torch.from_numpy(v.astype(np.float64))
+    opt.step()
+    np.testing.assert_allclose(out["m64"], st["exp_avg"].numpy(), rtol=1e-14, atol=0)
+    np.testing.assert_allclose(out["v64"], st["exp_avg_sq"].numpy(), rtol=1e-14, atol=0)
+    np.testing.assert_allclose(out["W64"], p.detach().numpy(), rtol=1e-13, atol=1e-17)
+
+
+def test_bf16_moment_storage_is_rne_of_fp64():
+    rng = np.random.default_rng(6)
+    G = rng.standard_normal((8, 32)) * 0.02
+    W = bf16_rand((8, 32), 0.02, 45)
+    m, v = _state(8, 32, MOMENT_BF16, 9, warm=True)
+    out = oracle.adamw(G, W, m, v, moment_dtype=MOMENT_BF16, step=100, **HP)
+    assert np.array_equal(out["m"], oracle.f64_to_bf16_bits(out["m64"]))
+    assert np.array_equal(out["v"], oracle.f64_to_bf16_bits(out["v64"]))
+    # warm state decoded from bf16 enters the recurrence
+    np.testing.assert_allclose(out["m64"], f32(0.9) * _decode(m, MOMENT_BF16) + (1 - f32(0.9)) * G,
+                               rtol=1e-15)
+
+
+def test_round_grad_to_bf16_variant():
+    """The two-kernel path with a bf16 gradient buffer sees RNE(G) (App. B truncation)."""
+    rng = np.random.default_rng(7)
+    G = rng.standard_normal((8, 16)) * 0.02
+    W = bf16_rand((8, 16), 0.02, 46)
+    z = np.zeros((8, 16), np.float32)
+    out = oracle.adamw(G, W, z, z, moment_dtype=MOMENT_F32, step=1, round_grad_to_bf16=True, **HP)
+    Gr = oracle.bf16_bits_to_f64(oracle.f64_to_bf16_bits(G))
+    assert not np.array_equal(Gr, G)
+    np.testing.assert_allclose(out["m64"], (1 - f32(0.9)) * Gr, rtol=1e-15)
+
+
+# ------------------------------------------------------------------------- int8 moments
+
+def test_i8_quantizer_invariants():
+    rng = np.random.default_rng(8)
+    d_out, d_in = 512 + 100, 24          # two full blocks and a ragged 100-row block
+    x = rng.standard_normal((d_out, d_in)) * 1e-3
+    x[256:512, 5] = 0.0                  # an all-zero block column
+    codes, scales = oracle.quantize_i8(x, second_moment=False)
+    assert scales.shape == (3, d_in)
+    assert codes.min() >= -127 and codes.max() <= 127
+    for b in range(3):
+        rows = slice(256 * b, min(256 * (b + 1), d_out))
+        for q in range(d_in):
+            col, cq, s = x[rows, q], codes[rows, q], float(scales[b, q])
+            a = np.abs(col.astype(np.float32)).max()
+            assert s == float(np.float32(a) / np.float32(127))
+            if a == 0:
+                assert s == 0 and not cq.any()
+                continue
+            assert np.abs(cq).max() == 127
+            assert np.abs(cq[np.argmax(np.abs(col))]) == 127
+            assert np.all(np.abs(col - s * cq.astype(np.float64)) <= s / 2 * (1 + 1e-6))
+
+
+def test_i8_second_moment_floor_and_sqrt_storage():
+    rng = np.random.default_rng(9)
+    v = np.abs(rng.standard_normal((256, 16)) * 1e-6)
+    v[3, 2] = 0.0
+    v[7, 2] = 1e-20                         # would quantize to 0 without the floor
+    codes, scales = oracle.quantize_i8(v, second_moment=True)
+    assert codes.min() >= 1 and codes.max() <= 127
+    r = np.sqrt(v)
+    np.testing.assert_allclose(scales[0], np.abs(r.astype(np.float32)).max(0) / np.float32(127), rtol=0)
+    dec = oracle.dequantize_i8(codes, scales, second_moment=True)
+    assert np.all(dec > 0)
+    big = r >= scales[0]                     # away from the floor the error is at most half a step
+    assert np.all(np.abs(np.sqrt(dec) - r)[big] <= (scales[0] / 2 * (1 + 1e-6) * np.ones_like(r))[big])
+
+
+def test_i8_first_moment_accumulated_error_bound():
+    """App. B: re-quantizing every step keeps |m_q - m| <= s/(2(1-b1)), s the largest scale."""
+    rng = np.random.default_rng(10)
+    d_out, d_in, b1 = 256, 8, 0.9
+    W = bf16_rand((d_out, d_in), 0.02, 47)
+    m_exact = np.zeros((d_out, d_in))
+    mq, ms = oracle.quantize_i8(m_exact, second_moment=False)
+    vq, vs = oracle.quantize_i8(np.full((d_out, d_in), 1e-6), second_moment=True)
+    smax = np.zeros(d_in)
+    for t in range(1, 41):
+        G = rng.standard_normal((d_out, d_in)) * 0.02
+        out = oracle.adamw(G, W, mq, vq, m_scale=ms, v_scale=vs, moment_dtype=MOMENT_I8, step=t,
+                           **dict(HP, beta1=b1))
+        m_exact = f32(b1) * m_exact + (1 - f32(b1)) * G
+        mq, vq, ms, vs = out["m"], out["v"], out["m_scale"], out["v_scale"]
+        smax = np.maximum(smax, ms[0])
+        err = np.abs(oracle.dequantize_i8(mq, ms, False) - m_exact)
+        assert np.all(err <= smax / (2 * (1 - f32(b1))) * (1 + 1e-4))
+
+
+def test_i8_step_weight_update_reads_unquantized_state():
+    """int8 mode: the new codes decode near m', and W' is the same as with fp32 moments."""
+    rng = np.random.default_rng(11)
+    d_out, d_in = 300, 16
+    G = rng.standard_normal((d_out, d_in)) * 0.02
+    W = bf16_rand((d_out, d_in), 0.02, 48)
+    m0 = rng.standard_normal((d_out, d_in)) * 1e-4
+    v0 = np.abs(rng.standard_normal((d_out, d_in))) * 1e-6
+    mq, ms = oracle.quantize_i8(m0, False)
+    vq, vs = oracle.quantize_i8(v0, True)
+    out8 = oracle.adamw(G, W, mq, vq, m_scale=ms, v_scale=vs, moment_dtype=MOMENT_I8, step=100,
+                        want_quotients=True, **HP)
+    # same decoded state as fp64 moments through the fp32-storage path -> same W64
+    md = oracle.dequantize_i8(mq, ms, False)
+    vd = oracle.dequantize_i8(vq, vs, True)
+    ref = oracle.adamw(G, W, md.astype(np.float32), vd.astype(np.float32), moment_dtype=MOMENT_F32,
+                       step=100, **HP)
+    # fp32 storage of the decoded state rounds it: allow that rounding only
+    np.testing.assert_allclose(out8["W64"], ref["W64"], rtol=1e-6, atol=1e-9)
+    dec = oracle.dequantize_i8(out8["m"], out8["m_scale"], False)
+    s = np.repeat(out8["m_scale"], 256, axis=0)[:d_out]
+    assert np.all(np.abs(dec - out8["m64"]) <= s / 2 * (1 + 1e-5))
+    assert np.all(np.abs(out8["qm"] - out8["m"]) <= 0.5 + 1e-6)
