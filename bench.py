@@ -1,0 +1,208 @@
+#!/usr/bin/env python3
+"""Benchmark: the fused weight-gradient + AdamW step over the Llama-3.1-8B linear layers.
+
+One "step" is one fused step (forge_linear_step) on every linear weight of the model:
+32 decoder layers x {q, k, v, o, gate, up, down} + lm_head, T = 512 tokens, bf16 W, m and
+v, launched back to back on one stream, all inputs resident in HBM (synthetic Gaussian
+data, seeded).  Printed value: algorithmic HBM bytes of a step / step time (GB/s).
+
+Prints one JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
+MFMA_BF16_PEAK_TFS = 2500.0    # dense bf16 MFMA, published
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def build_workload(wl, device, moment_override=None):
+    """Device tensors for every matrix of the workload, drawn on the GPU from seeded generators."""
+    import torch
+    from paper_2606_22932_amd import synth
+    mats = []
+    for mat in wl.matrices:
+        X, dY = synth.activations(wl.T, mat, wl, wl.steps[0], device=device)
+        W = synth.weight(mat, wl, device=device)
+        if wl.moment == "i8":
+            mq, vq, ms, vs = synth.random_i8_state(mat, wl, device=device)
+            mats.append(dict(mat=mat, X=X, dY=dY, W=W, m=mq, v=vq, ms=ms, vs=vs))
+        else:
+            dt = torch.bfloat16 if wl.moment == "bf16" else torch.float32
+            m, v = synth.warm_moments(mat, wl, device=device, dtype=dt)
+            mats.append(dict(mat=mat, X=X, dY=dY, W=W, m=m, v=v, ms=None, vs=None))
+    return mats
+
+
+def time_steps(mats, wl, fn, steps, warmup, step0):
+    """Run `warmup` untimed steps, then `steps` timed steps.  Returns (total ms, per-launch ms list)."""
+    import torch
+    for i in range(warmup):
+        for d in mats:
+            fn(d, step0 + i)
+    torch.cuda.synchronize()
+    n = len(mats)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n + 1)] for _ in range(steps)]
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start.record()
+    for s in range(steps):
+        e = evs[s]
+        e[0].record()
+        for j, d in enumerate(mats):
+            fn(d, step0 + warmup + s)
+            e[j + 1].record()
+    end.record()
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) * 1e3
+    total = start.elapsed_time(end)
+    per_launch = [[evs[s][j].elapsed_time(evs[s][j + 1]) for j in range(n)] for s in range(steps)]
+    return total, per_launch, wall
+
+
+def cpu_baseline(wl):
+    """The oracle on a bounded sample: one full o_proj-shaped matrix (4096 x 4096, T=512)."""
+    import numpy as np
+    import oracle
+    import torch
+    from paper_2606_22932_amd import accounting, synth
+    mat = synth.Matrix("L0.o", 4096, 4096, 103)
+    X, dY = synth.activations(wl.T, mat, wl, wl.steps[0])
+    W = synth.weight(mat, wl)
+    m, v = synth.warm_moments(mat, wl, dtype=torch.bfloat16)
+    b = lambda t: t.contiguous().view(torch.int16).numpy().view(np.uint16)
+    args = (b(X), b(dY), b(W), b(m), b(v))
+    t0 = time.perf_counter()
+    oracle.linear_step(*args, moment_dtype=oracle.MOMENT_BF16, step=wl.steps[0], **wl.hyper)
+    dt = time.perf_counter() - t0
+    gb = accounting.fused_bytes(wl.T, 4096, 4096, "bf16") / 1e9
+    return dict(value=round(gb / dt, 4), unit="GB/s", cores=oracle.num_threads(), kind="oracle",
+                seconds=round(dt, 3),
+                sample="one 4096x4096 layer (L0.o_proj, T=512, bf16 moments) of the sweep, "
+                       "fp64 oracle; value = its algorithmic bytes / oracle wall time")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="sweep", choices=["sweep", "o_proj", "mlp", "mlp_i8"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-unfused", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures the fused step on one GPU only: the step has no cross-GPU "
+              "work (run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2606_22932_amd import accounting, forge, synth
+
+    forge.lib()                                  # fails loudly if the HIP library is not built
+    device = torch.device("cuda:0")
+    torch.cuda.set_device(device)
+    wl = synth.WORKLOADS[args.workload]
+    log(f"building {args.workload}: {len(wl.matrices)} matrices")
+    mats = build_workload(wl, device)
+    torch.cuda.synchronize()
+    hp = wl.hyper
+    T = wl.T
+
+    def fused(d, t):
+        forge.forge_linear_step(d["X"], d["dY"], d["W"], d["m"], d["v"], d["ms"], d["vs"], step=t, **hp)
+
+    fused_b = sum(accounting.fused_bytes(T, d["mat"].d_in, d["mat"].d_out, wl.moment) for d in mats)
+    flops = sum(accounting.gemm_flops(T, d["mat"].d_in, d["mat"].d_out) for d in mats)
+    log("timing fused")
+    total, per_launch, wall = time_steps(mats, wl, fused, args.steps, args.warmup, wl.steps[0])
+    ms = total / args.steps
+    launches = [x for s in per_launch for x in s]
+    avg_launch_ms = sum(launches) / len(launches)
+    kern_gbs = fused_b * args.steps / (sum(launches) * 1e-3) / 1e9
+    value = fused_b / (ms * 1e-3) / 1e9
+    log(f"fused: {ms:.3f} ms/step, {value:.1f} GB/s, kernel-time {kern_gbs:.1f} GB/s, "
+        f"MFMA {flops / (ms * 1e-3) / 1e12:.1f} TF/s, wall {wall:.1f} ms")
+
+    out = {
+        "metric": "fused dW+AdamW step: HBM GB/s & % roofline; ms per Llama-8B linear sweep",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded Gaussian X, dY, W, warm m, v; generated on the GPU)",
+        "config": {
+            "workload": {"sweep": "Llama-3.1-8B linear-layer sweep: 32 x {q,k,v,o,gate,up,down} + lm_head, T=512, bf16 W/m/v",
+                         "o_proj": "Llama-3.1-8B o_proj 4096x4096, T=512, bf16 W/m/v",
+                         "mlp": "Llama-3.1-8B gate/up/down, T=512, bf16 W/m/v",
+                         "mlp_i8": "Llama-3.1-8B gate/up/down, T=512, int8 m/v"}[args.workload],
+            "T": T, "matrices": len(mats),
+            "params": sum(d["mat"].d_in * d["mat"].d_out for d in mats),
+            "moments": wl.moment, "algorithmic_bytes_per_step": fused_b,
+        },
+        "roofline": {
+            "bound": "hbm",
+            "achieved": round(kern_gbs, 2),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(kern_gbs / HBM_PEAK_GBS, 4),
+            "traffic": None,
+            "kernel": "fused_kernel (forge_linear_step)",
+            "avg_launch_us": round(avg_launch_ms * 1e3, 3),
+            "launches_per_step": len(mats),
+        },
+        "mfma_tflops": round(flops / (ms * 1e-3) / 1e12, 2),
+        "mfma_frac": round(flops / (ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFS, 4),
+    }
+
+    if not args.no_unfused and wl.moment != "f32":
+        biggest = max(d["mat"].d_in * d["mat"].d_out for d in mats)
+        G_ws = torch.empty(biggest, dtype=torch.bfloat16, device=device)
+
+        def unfused(d, t):
+            forge.forge_linear_step_unfused(d["X"], d["dY"], d["W"], d["m"], d["v"], d["ms"], d["vs"],
+                                            G_ws=G_ws, step=t, **hp)
+
+        log("timing unfused (GEMM stores bf16 G, then the optimizer kernel)")
+        ut, _, _ = time_steps(mats, wl, unfused, args.steps, args.warmup, wl.steps[0] + 1000)
+        ums = ut / args.steps
+        ub = sum(accounting.unfused_bytes(T, d["mat"].d_in, d["mat"].d_out, wl.moment, "bf16") for d in mats)
+        out["unfused"] = {"ms_per_step": round(ums, 4), "algorithmic_bytes_per_step": ub,
+                          "GBs_of_fused_bytes": round(fused_b / (ums * 1e-3) / 1e9, 2),
+                          "speedup_fused_over_unfused": round(ums / ms, 4)}
+        log(f"unfused: {ums:.3f} ms/step -> fused speedup {ums / ms:.3f}x")
+        del G_ws
+
+    if not args.no_cpu_baseline:
+        del mats
+        torch.cuda.empty_cache()
+        log("timing the CPU oracle on its sample")
+        out["cpu_baseline"] = cpu_baseline(synth.WORKLOADS["o_proj"])
+        log(f"cpu baseline: {out['cpu_baseline']}")
+
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

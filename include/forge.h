@@ -1,0 +1,142 @@
+/*
+ * forge.h -- C ABI of the MI355X (gfx950) fused weight-gradient + optimizer step.
+ *
+ * The operation (FORGE, Sec. 2.1-2.2, Eq. wgrad, Eq. tile, Algorithm 1): for a linear
+ * layer Y = X W^T with weight W [d_out, d_in], activations X [T, d_in] and upstream
+ * gradient dY [T, d_out], the weight gradient is G = dY^T X [d_out, d_in].  One call
+ * forms G tile by tile in fp32 registers and applies AdamW to each tile right there:
+ *
+ *     m <- beta1 m + (1 - beta1) G
+ *     v <- beta2 v + (1 - beta2) G*G
+ *     W <- (1 - lr*wd) W - lr * (m / (1 - beta1^t)) / (sqrt(v / (1 - beta2^t)) + eps)
+ *
+ * and writes back only W, m and v; G itself is never stored.
+ *
+ * Conventions shared by every entry point
+ * ----------------------------------------
+ * - All tensors are row-major and contiguous.  bf16 is the 16-bit brain float (top half
+ *   of an IEEE fp32).  Pointers are device pointers (HIP), owned by the caller; the
+ *   library allocates no device memory and keeps no state between calls.
+ * - W, m, v (and the int8 scales) are updated in place; X and dY are read only.
+ * - `stream` is a hipStream_t passed as void* (NULL = the default stream).  Calls only
+ *   enqueue work: they return once the kernels are launched.  Faults inside a kernel
+ *   surface at the caller's next synchronisation.
+ * - Arguments are validated on the host before any HIP call, in this order: dtype codes,
+ *   shapes (negative -> INVALID_SHAPE, unsupported -> UNSUPPORTED_SHAPE), the empty
+ *   problem (d_in == 0 or d_out == 0 returns FORGE_OK with no launch), pointers,
+ *   hyper-parameters, alignment, aliasing.  Validation never touches the GPU, so every
+ *   error path can be exercised on a machine without one.
+ * - Supported shapes: T >= 0 (T == 0 means a zero gradient), d_in and d_out multiples of
+ *   8, and every tensor below 2^31 elements.  Ragged tiles (sizes not multiples of the
+ *   tile) and ragged token counts are handled inside the kernels.
+ * - NaN / Inf inputs are not checked; they propagate.
+ * - Precondition (Algorithm 1, first line; the ordering remark of App. A): the layer's
+ *   input gradient dX = dY W must already have been computed from the pre-update W.
+ */
+#ifndef FORGE_H
+#define FORGE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Storage type of the optimizer moments m and v. */
+typedef enum {
+    FORGE_MOMENT_F32 = 0,  /* fp32 m and v */
+    FORGE_MOMENT_BF16 = 1, /* bf16 m and v (round-to-nearest-even stores) */
+    FORGE_MOMENT_I8 = 2    /* int8 codes with one fp32 absmax scale per 256 rows of d_out and
+                              per column: m = s_m * q_m, v = (s_v * q_v)^2 (the code stores
+                              sqrt(v)); scales are [ceil(d_out/256), d_in] fp32.  The int8
+                              block scheme follows App. B (re-quantised every step, second
+                              moment kept away from zero: its codes are at least 1 in any
+                              non-zero block). */
+} forge_moment_dtype;
+
+/* Element type of a materialised gradient (only the two-kernel path stores one). */
+typedef enum { FORGE_GRAD_BF16 = 0, FORGE_GRAD_F32 = 1 } forge_grad_dtype;
+
+typedef enum {
+    FORGE_OK = 0,
+    FORGE_ERR_NULL_POINTER = 1,      /* a required pointer is NULL */
+    FORGE_ERR_INVALID_SHAPE = 2,     /* a negative size */
+    FORGE_ERR_UNSUPPORTED_SHAPE = 3, /* d_in or d_out not a multiple of 8, or a tensor >= 2^31 elements */
+    FORGE_ERR_INVALID_HYPERPARAM = 4,/* step < 1, beta outside [0,1), eps <= 0, lr < 0, non-finite value */
+    FORGE_ERR_INVALID_DTYPE = 5,     /* unknown moment or gradient dtype code */
+    FORGE_ERR_MISALIGNED = 6,        /* a tensor pointer not 16-byte aligned */
+    FORGE_ERR_ALIASING = 7,          /* an output overlaps another tensor */
+    FORGE_ERR_NO_DEVICE = 8,         /* no usable gfx950 device is current */
+    FORGE_ERR_LAUNCH = 9             /* the kernel launch failed (hipGetLastError) */
+} forge_status;
+
+/*
+ * forge_linear_step -- the fused step (Algorithm 1 over every tile of W).
+ *
+ *   X        bf16 [T, d_in]            activations (may be NULL when T == 0)
+ *   dY       bf16 [T, d_out]           upstream gradient (may be NULL when T == 0)
+ *   W        bf16 [d_out, d_in]        weight, in/out
+ *   m, v     [d_out, d_in] moments in `moment_dtype` (int8: codes), in/out
+ *   m_scale, v_scale   int8 only: fp32 [ceil(d_out/256), d_in], in/out; ignored otherwise
+ *   step     t >= 1, the step being taken (bias corrections 1 - beta^t)
+ *   lr, beta1, beta2, eps, weight_decay   AdamW hyper-parameters (Algorithm 1 notation
+ *            eta, beta1, beta2, epsilon, lambda); decay is decoupled: W *= 1 - lr*wd.
+ *
+ * The gradient is accumulated in fp32 from bf16 products; the update runs in fp32; W is
+ * stored to bf16 with round-to-nearest-even.  No gradient byte is written to memory.
+ */
+forge_status forge_linear_step(const void *X, const void *dY, void *W, void *m, void *v,
+                               float *m_scale, float *v_scale, int64_t T, int64_t d_in,
+                               int64_t d_out, int32_t moment_dtype, float lr, float beta1,
+                               float beta2, float eps, float weight_decay, int64_t step,
+                               void *stream);
+
+/*
+ * forge_wgrad -- the weight-gradient GEMM alone, storing G = dY^T X (Eq. wgrad) to
+ * `G` [d_out, d_in] in `grad_dtype` (bf16 with round-to-nearest-even, or fp32).  This is
+ * the first kernel of the two-kernel comparison path and the store-G control of App. D.
+ */
+forge_status forge_wgrad(const void *X, const void *dY, void *G, int64_t T, int64_t d_in,
+                         int64_t d_out, int32_t grad_dtype, void *stream);
+
+/*
+ * forge_adamw -- the stand-alone optimizer kernel: one AdamW step (Algorithm 1, state
+ * update then weight update) reading a materialised gradient `G` [d_out, d_in] in
+ * `grad_dtype`.  Arguments as in forge_linear_step.  G is read only.
+ */
+forge_status forge_adamw(const void *G, int32_t grad_dtype, void *W, void *m, void *v,
+                         float *m_scale, float *v_scale, int64_t d_in, int64_t d_out,
+                         int32_t moment_dtype, float lr, float beta1, float beta2, float eps,
+                         float weight_decay, int64_t step, void *stream);
+
+/*
+ * forge_linear_step_unfused -- the same step as forge_linear_step done the conventional
+ * way: forge_wgrad writes G into the caller's workspace `G_ws` (d_out*d_in elements of
+ * `grad_dtype`), then forge_adamw consumes it, both on `stream`.  It exists to measure
+ * the HBM traffic that fusion removes (Sec. 2.2, "Memory and bandwidth": the gradient's
+ * write and read).  With a bf16 workspace the optimizer sees G rounded to bf16 (the
+ * truncation discussed in App. B).
+ */
+forge_status forge_linear_step_unfused(const void *X, const void *dY, void *W, void *m,
+                                       void *v, float *m_scale, float *v_scale, int64_t T,
+                                       int64_t d_in, int64_t d_out, int32_t moment_dtype,
+                                       float lr, float beta1, float beta2, float eps,
+                                       float weight_decay, int64_t step, void *G_ws,
+                                       int32_t grad_dtype, void *stream);
+
+/* Static description of a status code (never NULL). */
+const char *forge_status_string(int32_t status);
+
+/*
+ * forge_query_tile -- the tile geometry the fused kernel uses for `moment_dtype`:
+ * rows of W (along d_out), columns (along d_in) and tokens per pipeline chunk.
+ * Any output pointer may be NULL.  Returns FORGE_ERR_INVALID_DTYPE for an unknown code.
+ */
+forge_status forge_query_tile(int32_t moment_dtype, int32_t *tile_rows, int32_t *tile_cols,
+                              int32_t *tile_tokens);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FORGE_H */

@@ -1,0 +1,323 @@
+// forge_api.cpp -- the C ABI declared in include/forge.h: argument validation (host only,
+// before any HIP call), the per-call scalars of Algorithm 1 computed in fp64, and the
+// kernel launches.
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <mutex>
+
+#include "forge.h"
+#include "forge_internal.h"
+
+using forge_impl::Args;
+using forge_impl::Hyper;
+
+namespace {
+
+constexpr int64_t kMaxElems = (int64_t(1) << 31) - 1;
+
+struct Range {
+    uintptr_t lo, hi;   // [lo, hi)
+};
+
+bool overlap(Range a, Range b) { return a.lo < b.hi && b.lo < a.hi; }
+
+Range range_of(const void *p, int64_t bytes)
+{
+    uintptr_t lo = reinterpret_cast<uintptr_t>(p);
+    return Range{lo, lo + static_cast<uintptr_t>(bytes)};
+}
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int64_t moment_bytes(int32_t md) { return md == FORGE_MOMENT_F32 ? 4 : md == FORGE_MOMENT_BF16 ? 2 : 1; }
+
+bool finite(float x) { return std::isfinite(x); }
+
+forge_status check_dtype_moment(int32_t md)
+{
+    return (md == FORGE_MOMENT_F32 || md == FORGE_MOMENT_BF16 || md == FORGE_MOMENT_I8)
+               ? FORGE_OK : FORGE_ERR_INVALID_DTYPE;
+}
+
+forge_status check_dtype_grad(int32_t gd)
+{
+    return (gd == FORGE_GRAD_BF16 || gd == FORGE_GRAD_F32) ? FORGE_OK : FORGE_ERR_INVALID_DTYPE;
+}
+
+// Shape rules; `empty` is set when there is nothing to update.
+forge_status check_shape(int64_t T, int64_t d_in, int64_t d_out, bool &empty)
+{
+    if (T < 0 || d_in < 0 || d_out < 0) return FORGE_ERR_INVALID_SHAPE;
+    if (d_in % 8 != 0 || d_out % 8 != 0) return FORGE_ERR_UNSUPPORTED_SHAPE;
+    if (T > kMaxElems || d_in > kMaxElems || d_out > kMaxElems) return FORGE_ERR_UNSUPPORTED_SHAPE;
+    if (d_in * d_out > kMaxElems || T * d_in > kMaxElems || T * d_out > kMaxElems)
+        return FORGE_ERR_UNSUPPORTED_SHAPE;
+    empty = (d_in == 0 || d_out == 0);
+    return FORGE_OK;
+}
+
+forge_status check_hyper(float lr, float b1, float b2, float eps, float wd, int64_t step)
+{
+    if (step < 1) return FORGE_ERR_INVALID_HYPERPARAM;
+    if (!finite(lr) || !finite(b1) || !finite(b2) || !finite(eps) || !finite(wd))
+        return FORGE_ERR_INVALID_HYPERPARAM;
+    if (!(b1 >= 0.0f && b1 < 1.0f) || !(b2 >= 0.0f && b2 < 1.0f)) return FORGE_ERR_INVALID_HYPERPARAM;
+    if (!(eps > 0.0f) || !(lr >= 0.0f)) return FORGE_ERR_INVALID_HYPERPARAM;
+    return FORGE_OK;
+}
+
+// Per-call scalars in fp64, rounded once to fp32 (Algorithm 1: bias corrections and the
+// decoupled decay factor).
+Hyper make_hyper(float lr, float b1, float b2, float eps, float wd, int64_t step)
+{
+    const double t = static_cast<double>(step);
+    const double bc1 = 1.0 - std::pow(static_cast<double>(b1), t);
+    const double bc2 = 1.0 - std::pow(static_cast<double>(b2), t);
+    Hyper h;
+    h.b1 = b1;
+    h.c1 = static_cast<float>(1.0 - static_cast<double>(b1));
+    h.b2 = b2;
+    h.c2 = static_cast<float>(1.0 - static_cast<double>(b2));
+    h.lr_bc1 = static_cast<float>(static_cast<double>(lr) / bc1);
+    h.inv_sqrt_bc2 = static_cast<float>(1.0 / std::sqrt(bc2));
+    h.eps = eps;
+    h.wdf = static_cast<float>(1.0 - static_cast<double>(lr) * static_cast<double>(wd));
+    return h;
+}
+
+// The optimizer-state tensors of one step: pointers, alignment and mutual disjointness.
+struct StateSet {
+    Range r[5];
+    int n = 0;
+};
+
+forge_status check_state(void *W, void *m, void *v, float *ms, float *vs, int64_t d_in,
+                         int64_t d_out, int32_t md, StateSet &out)
+{
+    if (!W || !m || !v) return FORGE_ERR_NULL_POINTER;
+    const bool i8 = (md == FORGE_MOMENT_I8);
+    if (i8 && (!ms || !vs)) return FORGE_ERR_NULL_POINTER;
+    if (!aligned16(W) || !aligned16(m) || !aligned16(v)) return FORGE_ERR_MISALIGNED;
+    if (i8 && (!aligned16(ms) || !aligned16(vs))) return FORGE_ERR_MISALIGNED;
+    const int64_t P = d_in * d_out;
+    out.r[0] = range_of(W, 2 * P);
+    out.r[1] = range_of(m, moment_bytes(md) * P);
+    out.r[2] = range_of(v, moment_bytes(md) * P);
+    out.n = 3;
+    if (i8) {
+        const int64_t nsc = ((d_out + 255) / 256) * d_in * 4;
+        out.r[3] = range_of(ms, nsc);
+        out.r[4] = range_of(vs, nsc);
+        out.n = 5;
+    }
+    for (int i = 0; i < out.n; ++i)
+        for (int j = i + 1; j < out.n; ++j)
+            if (overlap(out.r[i], out.r[j])) return FORGE_ERR_ALIASING;
+    return FORGE_OK;
+}
+
+bool disjoint_from(const StateSet &s, Range x)
+{
+    for (int i = 0; i < s.n; ++i)
+        if (overlap(s.r[i], x)) return false;
+    return true;
+}
+
+forge_status check_inputs(const void *X, const void *dY, int64_t T, int64_t d_in, int64_t d_out)
+{
+    if (T == 0) return FORGE_OK;
+    if (!X || !dY) return FORGE_ERR_NULL_POINTER;
+    if (!aligned16(X) || !aligned16(dY)) return FORGE_ERR_MISALIGNED;
+    (void)d_in;
+    (void)d_out;
+    return FORGE_OK;
+}
+
+// The current device must be a gfx950; the answer is cached per device ordinal.
+forge_status check_device()
+{
+    static std::mutex mu;
+    static int known[64] = {0};   // 0 unknown, 1 ok, 2 not ok
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) {
+        (void)hipGetLastError();
+        return FORGE_ERR_NO_DEVICE;
+    }
+    if (dev >= 64) return FORGE_ERR_NO_DEVICE;
+    std::lock_guard<std::mutex> lock(mu);
+    if (known[dev] == 0) {
+        hipDeviceProp_t prop;
+        if (hipGetDeviceProperties(&prop, dev) != hipSuccess) {
+            (void)hipGetLastError();
+            return FORGE_ERR_NO_DEVICE;
+        }
+        known[dev] = (std::strncmp(prop.gcnArchName, "gfx950", 6) == 0) ? 1 : 2;
+    }
+    return known[dev] == 1 ? FORGE_OK : FORGE_ERR_NO_DEVICE;
+}
+
+forge_status from_hip(hipError_t e)
+{
+    if (e == hipSuccess) return FORGE_OK;
+    if (e == hipErrorNoDevice || e == hipErrorInvalidDevice) return FORGE_ERR_NO_DEVICE;
+    return FORGE_ERR_LAUNCH;
+}
+
+Args base_args(const void *X, const void *dY, int64_t T, int64_t d_in, int64_t d_out)
+{
+    Args a;
+    std::memset(&a, 0, sizeof a);
+    a.X = static_cast<const uint16_t *>(X);
+    a.dY = static_cast<const uint16_t *>(dY);
+    a.T = static_cast<int>(T);
+    a.d_in = static_cast<int>(d_in);
+    a.d_out = static_cast<int>(d_out);
+    return a;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *forge_status_string(int32_t s)
+{
+    switch (s) {
+    case FORGE_OK: return "FORGE_OK: success";
+    case FORGE_ERR_NULL_POINTER: return "FORGE_ERR_NULL_POINTER: a required pointer is NULL";
+    case FORGE_ERR_INVALID_SHAPE: return "FORGE_ERR_INVALID_SHAPE: a size is negative";
+    case FORGE_ERR_UNSUPPORTED_SHAPE:
+        return "FORGE_ERR_UNSUPPORTED_SHAPE: d_in and d_out must be multiples of 8 and every tensor below 2^31 elements";
+    case FORGE_ERR_INVALID_HYPERPARAM:
+        return "FORGE_ERR_INVALID_HYPERPARAM: need step >= 1, 0 <= beta < 1, eps > 0, lr >= 0, all finite";
+    case FORGE_ERR_INVALID_DTYPE: return "FORGE_ERR_INVALID_DTYPE: unknown moment or gradient dtype code";
+    case FORGE_ERR_MISALIGNED: return "FORGE_ERR_MISALIGNED: tensor pointers must be 16-byte aligned";
+    case FORGE_ERR_ALIASING: return "FORGE_ERR_ALIASING: an output tensor overlaps another tensor";
+    case FORGE_ERR_NO_DEVICE: return "FORGE_ERR_NO_DEVICE: no gfx950 device is current";
+    case FORGE_ERR_LAUNCH: return "FORGE_ERR_LAUNCH: kernel launch failed";
+    default: return "unknown forge_status";
+    }
+}
+
+forge_status forge_query_tile(int32_t md, int32_t *rows, int32_t *cols, int32_t *tokens)
+{
+    if (check_dtype_moment(md) != FORGE_OK) return FORGE_ERR_INVALID_DTYPE;
+    const forge_impl::TileShape t = forge_impl::tile_shape(md);
+    if (rows) *rows = t.rows;
+    if (cols) *cols = t.cols;
+    if (tokens) *tokens = t.tokens;
+    return FORGE_OK;
+}
+
+forge_status forge_linear_step(const void *X, const void *dY, void *W, void *m, void *v,
+                               float *m_scale, float *v_scale, int64_t T, int64_t d_in,
+                               int64_t d_out, int32_t md, float lr, float beta1, float beta2,
+                               float eps, float weight_decay, int64_t step, void *stream)
+{
+    forge_status s;
+    bool empty = false;
+    if ((s = check_dtype_moment(md)) != FORGE_OK) return s;
+    if ((s = check_shape(T, d_in, d_out, empty)) != FORGE_OK) return s;
+    if (empty) return FORGE_OK;
+    StateSet st;
+    if ((s = check_inputs(X, dY, T, d_in, d_out)) != FORGE_OK) return s;
+    if ((s = check_state(W, m, v, m_scale, v_scale, d_in, d_out, md, st)) != FORGE_OK) return s;
+    if ((s = check_hyper(lr, beta1, beta2, eps, weight_decay, step)) != FORGE_OK) return s;
+    if (T > 0 && (!disjoint_from(st, range_of(X, 2 * T * d_in)) ||
+                  !disjoint_from(st, range_of(dY, 2 * T * d_out))))
+        return FORGE_ERR_ALIASING;
+    if ((s = check_device()) != FORGE_OK) return s;
+
+    Args a = base_args(X, dY, T, d_in, d_out);
+    a.W = static_cast<uint16_t *>(W);
+    a.m = m;
+    a.v = v;
+    a.ms = m_scale;
+    a.vs = v_scale;
+    a.h = make_hyper(lr, beta1, beta2, eps, weight_decay, step);
+    return from_hip(forge_impl::launch_fused(a, md, static_cast<hipStream_t>(stream)));
+}
+
+forge_status forge_wgrad(const void *X, const void *dY, void *G, int64_t T, int64_t d_in,
+                         int64_t d_out, int32_t gd, void *stream)
+{
+    forge_status s;
+    bool empty = false;
+    if ((s = check_dtype_grad(gd)) != FORGE_OK) return s;
+    if ((s = check_shape(T, d_in, d_out, empty)) != FORGE_OK) return s;
+    if (empty) return FORGE_OK;
+    if ((s = check_inputs(X, dY, T, d_in, d_out)) != FORGE_OK) return s;
+    if (!G) return FORGE_ERR_NULL_POINTER;
+    if (!aligned16(G)) return FORGE_ERR_MISALIGNED;
+    const Range rg = range_of(G, (gd == FORGE_GRAD_F32 ? 4 : 2) * d_in * d_out);
+    if (T > 0 && (overlap(rg, range_of(X, 2 * T * d_in)) || overlap(rg, range_of(dY, 2 * T * d_out))))
+        return FORGE_ERR_ALIASING;
+    if ((s = check_device()) != FORGE_OK) return s;
+
+    Args a = base_args(X, dY, T, d_in, d_out);
+    a.G = G;
+    return from_hip(forge_impl::launch_wgrad(a, gd == FORGE_GRAD_F32, static_cast<hipStream_t>(stream)));
+}
+
+forge_status forge_adamw(const void *G, int32_t gd, void *W, void *m, void *v, float *m_scale,
+                         float *v_scale, int64_t d_in, int64_t d_out, int32_t md, float lr,
+                         float beta1, float beta2, float eps, float weight_decay, int64_t step,
+                         void *stream)
+{
+    forge_status s;
+    bool empty = false;
+    if ((s = check_dtype_moment(md)) != FORGE_OK) return s;
+    if ((s = check_dtype_grad(gd)) != FORGE_OK) return s;
+    if ((s = check_shape(0, d_in, d_out, empty)) != FORGE_OK) return s;
+    if (empty) return FORGE_OK;
+    if (!G) return FORGE_ERR_NULL_POINTER;
+    StateSet st;
+    if ((s = check_state(W, m, v, m_scale, v_scale, d_in, d_out, md, st)) != FORGE_OK) return s;
+    if (!aligned16(G)) return FORGE_ERR_MISALIGNED;
+    if ((s = check_hyper(lr, beta1, beta2, eps, weight_decay, step)) != FORGE_OK) return s;
+    if (!disjoint_from(st, range_of(G, (gd == FORGE_GRAD_F32 ? 4 : 2) * d_in * d_out)))
+        return FORGE_ERR_ALIASING;
+    if ((s = check_device()) != FORGE_OK) return s;
+
+    Args a = base_args(nullptr, nullptr, 0, d_in, d_out);
+    a.G = const_cast<void *>(G);
+    a.W = static_cast<uint16_t *>(W);
+    a.m = m;
+    a.v = v;
+    a.ms = m_scale;
+    a.vs = v_scale;
+    a.h = make_hyper(lr, beta1, beta2, eps, weight_decay, step);
+    return from_hip(forge_impl::launch_adamw(a, md, gd == FORGE_GRAD_F32, static_cast<hipStream_t>(stream)));
+}
+
+forge_status forge_linear_step_unfused(const void *X, const void *dY, void *W, void *m, void *v,
+                                       float *m_scale, float *v_scale, int64_t T, int64_t d_in,
+                                       int64_t d_out, int32_t md, float lr, float beta1,
+                                       float beta2, float eps, float weight_decay, int64_t step,
+                                       void *G_ws, int32_t gd, void *stream)
+{
+    forge_status s;
+    bool empty = false;
+    if ((s = check_dtype_moment(md)) != FORGE_OK) return s;
+    if ((s = check_dtype_grad(gd)) != FORGE_OK) return s;
+    if ((s = check_shape(T, d_in, d_out, empty)) != FORGE_OK) return s;
+    if (empty) return FORGE_OK;
+    StateSet st;
+    if ((s = check_inputs(X, dY, T, d_in, d_out)) != FORGE_OK) return s;
+    if ((s = check_state(W, m, v, m_scale, v_scale, d_in, d_out, md, st)) != FORGE_OK) return s;
+    if (!G_ws) return FORGE_ERR_NULL_POINTER;
+    if (!aligned16(G_ws)) return FORGE_ERR_MISALIGNED;
+    if ((s = check_hyper(lr, beta1, beta2, eps, weight_decay, step)) != FORGE_OK) return s;
+    const Range rg = range_of(G_ws, (gd == FORGE_GRAD_F32 ? 4 : 2) * d_in * d_out);
+    if (!disjoint_from(st, rg)) return FORGE_ERR_ALIASING;
+    if (T > 0) {
+        const Range rx = range_of(X, 2 * T * d_in), ry = range_of(dY, 2 * T * d_out);
+        if (!disjoint_from(st, rx) || !disjoint_from(st, ry) || overlap(rg, rx) || overlap(rg, ry))
+            return FORGE_ERR_ALIASING;
+    }
+    if ((s = forge_wgrad(X, dY, G_ws, T, d_in, d_out, gd, stream)) != FORGE_OK) return s;
+    return forge_adamw(G_ws, gd, W, m, v, m_scale, v_scale, d_in, d_out, md, lr, beta1, beta2,
+                       eps, weight_decay, step, stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,48 @@
+// Internal interface between the C-ABI layer (forge_api.cpp) and the HIP kernels
+// (forge_kernels.hip).  Not installed; callers use include/forge.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace forge_impl {
+
+// Scalars of one AdamW step, precomputed on the host in fp64 and rounded to fp32
+// (Algorithm 1: the state recurrences and the bias-corrected, decoupled update).
+struct Hyper {
+    float b1, c1;          // beta1, 1 - beta1
+    float b2, c2;          // beta2, 1 - beta2
+    float lr_bc1;          // lr / (1 - beta1^t)
+    float inv_sqrt_bc2;    // 1 / sqrt(1 - beta2^t)
+    float eps;
+    float wdf;             // 1 - lr * weight_decay
+};
+
+// Everything a launch needs; passed by value as the kernel argument.
+struct Args {
+    const uint16_t *X;     // bf16 [T, d_in]
+    const uint16_t *dY;    // bf16 [T, d_out]
+    uint16_t *W;           // bf16 [d_out, d_in]
+    void *m, *v;           // moments, storage per moment dtype
+    float *ms, *vs;        // int8 block scales [ceil(d_out/256), d_in]
+    void *G;               // materialised gradient (two-kernel path only)
+    int T, d_in, d_out;
+    int tiles_p, tiles_q;  // tile grid (along d_out, along d_in)
+    int group_p;           // raster group height in tiles (L2 reuse of operand slabs)
+    Hyper h;
+};
+
+enum MomentKind { MK_F32 = 0, MK_BF16 = 1, MK_I8 = 2 };
+enum EpiKind { EPI_ADAMW = 0, EPI_STORE_BF16 = 1, EPI_STORE_F32 = 2 };
+
+struct TileShape { int rows, cols, tokens; };
+
+// Tile geometry used for a moment kind (fused step and stand-alone optimizer alike).
+TileShape tile_shape(int moment_kind);
+
+// Launchers; they return the hipError_t of the launch.
+hipError_t launch_fused(const Args &a, int moment_kind, hipStream_t stream);
+hipError_t launch_wgrad(const Args &a, int grad_f32, hipStream_t stream);
+hipError_t launch_adamw(const Args &a, int moment_kind, int grad_f32, hipStream_t stream);
+
+}  // namespace forge_impl

@@ -1,0 +1,187 @@
+"""Python binding of the C ABI in ``include/forge.h`` (argument marshalling only).
+
+Every function here has the name of the C entry point it calls.  Tensors are torch
+tensors on the current HIP device; their data pointers, shapes and the current torch
+stream are passed through ctypes.  All arithmetic runs in the HIP kernels of
+``libforge.so``; there is no fallback: if the library is not built, calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+import threading
+
+from . import build as _build
+
+FORGE_MOMENT_F32, FORGE_MOMENT_BF16, FORGE_MOMENT_I8 = 0, 1, 2
+FORGE_GRAD_BF16, FORGE_GRAD_F32 = 0, 1
+
+STATUS = {
+    0: "FORGE_OK", 1: "FORGE_ERR_NULL_POINTER", 2: "FORGE_ERR_INVALID_SHAPE",
+    3: "FORGE_ERR_UNSUPPORTED_SHAPE", 4: "FORGE_ERR_INVALID_HYPERPARAM",
+    5: "FORGE_ERR_INVALID_DTYPE", 6: "FORGE_ERR_MISALIGNED", 7: "FORGE_ERR_ALIASING",
+    8: "FORGE_ERR_NO_DEVICE", 9: "FORGE_ERR_LAUNCH",
+}
+HEADER = os.path.join(_build.ROOT, "include", "forge.h")
+
+
+class ForgeError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        self.name = STATUS.get(code, "unknown")
+        super().__init__(f"{where}: {forge_status_string(code)}")
+
+
+_lock = threading.Lock()
+_lib = None
+
+_P, _I64, _I32, _F = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_float
+_SIGS = {
+    "forge_linear_step": [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I32, _F, _F, _F, _F, _F, _I64, _P],
+    "forge_wgrad": [_P, _P, _P, _I64, _I64, _I64, _I32, _P],
+    "forge_adamw": [_P, _I32, _P, _P, _P, _P, _P, _I64, _I64, _I32, _F, _F, _F, _F, _F, _I64, _P],
+    "forge_linear_step_unfused": [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I32, _F, _F, _F, _F,
+                                  _F, _I64, _P, _I32, _P],
+    "forge_status_string": [_I32],
+    "forge_query_tile": [_I32, ctypes.POINTER(_I32), ctypes.POINTER(_I32), ctypes.POINTER(_I32)],
+}
+
+
+def lib():
+    """The loaded ``libforge.so`` (raises if it has not been built)."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(_build.LIB):
+                raise RuntimeError(
+                    f"{_build.LIB} is not built: run `python -m paper_2606_22932_amd.build` "
+                    "(or __graft_entry__.build()) first; there is no non-HIP fallback")
+            L = ctypes.CDLL(_build.LIB)
+            for name, args in _SIGS.items():
+                fn = getattr(L, name)
+                fn.argtypes = args
+                fn.restype = ctypes.c_char_p if name == "forge_status_string" else ctypes.c_int32
+            _lib = L
+    return _lib
+
+
+def header_functions():
+    """Names of the functions ``include/forge.h`` declares."""
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(forge_[a-z_0-9]+)\s*\(", text)))
+
+
+def forge_status_string(code: int) -> str:
+    return lib().forge_status_string(int(code)).decode()
+
+
+def forge_query_tile(moment_dtype: int):
+    r, c, t = _I32(), _I32(), _I32()
+    st = lib().forge_query_tile(int(moment_dtype), ctypes.byref(r), ctypes.byref(c), ctypes.byref(t))
+    _check(st, "forge_query_tile")
+    return r.value, c.value, t.value
+
+
+# ----------------------------------------------------------------------------- marshalling
+
+def _check(status: int, where: str):
+    if status != 0:
+        raise ForgeError(status, where)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream, ref):
+    if stream is not None:
+        return ctypes.c_void_p(int(stream))
+    import torch
+    return ctypes.c_void_p(torch.cuda.current_stream(ref.device).cuda_stream)
+
+
+def _moment_code(m):
+    import torch
+    codes = {torch.float32: FORGE_MOMENT_F32, torch.bfloat16: FORGE_MOMENT_BF16, torch.int8: FORGE_MOMENT_I8}
+    if m.dtype not in codes:
+        raise TypeError(f"moments must be float32, bfloat16 or int8, got {m.dtype}")
+    return codes[m.dtype]
+
+
+def _grad_code(G):
+    import torch
+    codes = {torch.bfloat16: FORGE_GRAD_BF16, torch.float32: FORGE_GRAD_F32}
+    if G.dtype not in codes:
+        raise TypeError(f"gradient must be bfloat16 or float32, got {G.dtype}")
+    return codes[G.dtype]
+
+
+def _dev(*ts):
+    for t in ts:
+        if t is not None:
+            if not t.is_cuda:
+                raise ValueError("forge tensors must live on a HIP device")
+            if not t.is_contiguous():
+                raise ValueError("forge tensors must be contiguous")
+
+
+def _shapes(X, dY, W):
+    import torch
+    if W.dtype != torch.bfloat16 or X.dtype != torch.bfloat16 or dY.dtype != torch.bfloat16:
+        raise TypeError("X, dY and W must be bfloat16")
+    T, d_in = X.shape
+    T2, d_out = dY.shape
+    if T2 != T or tuple(W.shape) != (d_out, d_in):
+        raise ValueError(f"shape mismatch: X {tuple(X.shape)}, dY {tuple(dY.shape)}, W {tuple(W.shape)}")
+    return T, d_in, d_out
+
+
+def forge_linear_step(X, dY, W, m, v, m_scale=None, v_scale=None, *, lr, beta1, beta2, eps,
+                      weight_decay, step, stream=None):
+    """The fused step: W, m, v (and int8 scales) updated in place; G is never stored."""
+    _dev(X, dY, W, m, v, m_scale, v_scale)
+    T, d_in, d_out = _shapes(X, dY, W)
+    st = lib().forge_linear_step(_ptr(X), _ptr(dY), _ptr(W), _ptr(m), _ptr(v), _ptr(m_scale),
+                                 _ptr(v_scale), T, d_in, d_out, _moment_code(m), lr, beta1, beta2,
+                                 eps, weight_decay, int(step), _stream(stream, W))
+    _check(st, "forge_linear_step")
+
+
+def forge_wgrad(X, dY, G, *, stream=None):
+    """G = dY^T X stored in G's dtype (bfloat16 or float32)."""
+    _dev(X, dY, G)
+    T, d_in = X.shape
+    d_out = dY.shape[1]
+    if tuple(G.shape) != (d_out, d_in):
+        raise ValueError("G must be [d_out, d_in]")
+    st = lib().forge_wgrad(_ptr(X), _ptr(dY), _ptr(G), T, d_in, d_out, _grad_code(G), _stream(stream, G))
+    _check(st, "forge_wgrad")
+
+
+def forge_adamw(G, W, m, v, m_scale=None, v_scale=None, *, lr, beta1, beta2, eps, weight_decay,
+                step, stream=None):
+    """The stand-alone optimizer kernel over a materialised gradient G."""
+    _dev(G, W, m, v, m_scale, v_scale)
+    d_out, d_in = W.shape
+    if tuple(G.shape) != (d_out, d_in):
+        raise ValueError("G must match W")
+    st = lib().forge_adamw(_ptr(G), _grad_code(G), _ptr(W), _ptr(m), _ptr(v), _ptr(m_scale),
+                           _ptr(v_scale), d_in, d_out, _moment_code(m), lr, beta1, beta2, eps,
+                           weight_decay, int(step), _stream(stream, W))
+    _check(st, "forge_adamw")
+
+
+def forge_linear_step_unfused(X, dY, W, m, v, m_scale=None, v_scale=None, *, G_ws, lr, beta1,
+                              beta2, eps, weight_decay, step, stream=None):
+    """GEMM writes G into G_ws, then the optimizer kernel reads it (same stream)."""
+    _dev(X, dY, W, m, v, m_scale, v_scale, G_ws)
+    T, d_in, d_out = _shapes(X, dY, W)
+    if G_ws.numel() < d_in * d_out:
+        raise ValueError("G_ws too small")
+    st = lib().forge_linear_step_unfused(_ptr(X), _ptr(dY), _ptr(W), _ptr(m), _ptr(v),
+                                         _ptr(m_scale), _ptr(v_scale), T, d_in, d_out,
+                                         _moment_code(m), lr, beta1, beta2, eps, weight_decay,
+                                         int(step), _ptr(G_ws), _grad_code(G_ws), _stream(stream, W))
+    _check(st, "forge_linear_step_unfused")
