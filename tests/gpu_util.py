@@ -79,10 +79,22 @@ def with_state(p: Problem, st: dict, dY=None) -> Problem:
     return q
 
 
+def gemm_error_bound(X: np.ndarray, dY: np.ndarray) -> np.ndarray:
+    """Bound on the fp32 accumulation error of any summation order of G: T 2^-24 |dY|^T |X|.
+
+    (A numpy product of absolute values, used only as an error scale.)"""
+    T = X.shape[0]
+    ax = np.abs(oracle.bf16_bits_to_f64(X))
+    ay = np.abs(oracle.bf16_bits_to_f64(dY))
+    return T * 2.0 ** -24 * (ay.T @ ax)
+
+
 def run_oracle(p: Problem, step: int, round_grad_to_bf16=False):
-    return oracle.linear_step(p.X, p.dY, p.W, p.m, p.v, moment_dtype=MOMENT_CODE[p.moment], step=step,
-                              m_scale=p.m_scale, v_scale=p.v_scale, round_grad_to_bf16=round_grad_to_bf16,
-                              want_quotients=True, **p.hp)
+    out = oracle.linear_step(p.X, p.dY, p.W, p.m, p.v, moment_dtype=MOMENT_CODE[p.moment], step=step,
+                             m_scale=p.m_scale, v_scale=p.v_scale, round_grad_to_bf16=round_grad_to_bf16,
+                             want_quotients=True, **p.hp)
+    out["EG"] = gemm_error_bound(p.X, p.dY)
+    return out
 
 
 def run_gpu(p: Problem, step: int, *, path="fused", grad="f32"):

@@ -1,0 +1,161 @@
+"""The C ABI boundary on the host: the library loads, exports what include/forge.h declares,
+and every documented validation error is returned before any HIP call.
+
+Pointers here are fake addresses: validation never dereferences them.  No test makes a
+call whose arguments are all valid (that would launch a kernel on a GPU machine).
+"""
+import ctypes
+import json
+import os
+
+import pytest
+
+from paper_2606_22932_amd import accounting, forge
+
+OK, NULLP, SHAPE, UNSUP, HYPER, DTYPE, MISAL, ALIAS, NODEV, LAUNCH = range(10)
+F32, BF16, I8 = 0, 1, 2
+HP = dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, wd=0.1, step=1)
+
+GiB = 1 << 30
+# well separated, 256-byte aligned fake device addresses
+BASE = {k: (i + 1) * 8 * GiB for i, k in enumerate(["X", "dY", "W", "m", "v", "ms", "vs", "G"])}
+
+
+def lib():
+    return forge.lib()
+
+
+def call_step(T=64, d_in=128, d_out=256, md=BF16, **over):
+    a = dict(BASE)
+    a.update({k: v for k, v in over.items() if k in a})
+    hp = dict(HP)
+    hp.update({k: v for k, v in over.items() if k in hp})
+    return lib().forge_linear_step(a["X"], a["dY"], a["W"], a["m"], a["v"], a["ms"], a["vs"], T, d_in, d_out,
+                                   md, hp["lr"], hp["beta1"], hp["beta2"], hp["eps"], hp["wd"], hp["step"], None)
+
+
+def call_unfused(T=64, d_in=128, d_out=256, md=BF16, gd=0, **over):
+    a = dict(BASE)
+    a.update({k: v for k, v in over.items() if k in a})
+    hp = dict(HP)
+    hp.update({k: v for k, v in over.items() if k in hp})
+    return lib().forge_linear_step_unfused(a["X"], a["dY"], a["W"], a["m"], a["v"], a["ms"], a["vs"], T, d_in,
+                                           d_out, md, hp["lr"], hp["beta1"], hp["beta2"], hp["eps"], hp["wd"],
+                                           hp["step"], a["G"], gd, None)
+
+
+def test_library_exports_every_header_function():
+    names = forge.header_functions()
+    assert set(names) >= {"forge_linear_step", "forge_linear_step_unfused", "forge_wgrad", "forge_adamw",
+                          "forge_status_string", "forge_query_tile"}
+    L = lib()
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_status_strings():
+    for code in range(10):
+        s = forge.forge_status_string(code)
+        assert s.startswith(forge.STATUS[code])
+    assert "unknown" in forge.forge_status_string(99)
+
+
+def test_query_tile():
+    assert forge.forge_query_tile(BF16)[0] % 8 == 0
+    rows, cols, tk = forge.forge_query_tile(I8)
+    assert rows == 256            # an int8 tile is exactly one scale block tall
+    r = ctypes.c_int32()
+    assert lib().forge_query_tile(7, ctypes.byref(r), None, None) == DTYPE
+
+
+def test_dtype_errors():
+    assert call_step(md=3) == DTYPE
+    assert call_step(md=-1) == DTYPE
+    assert call_unfused(gd=2) == DTYPE
+    assert lib().forge_wgrad(BASE["X"], BASE["dY"], BASE["G"], 8, 8, 8, 5, None) == DTYPE
+
+
+def test_shape_errors():
+    assert call_step(T=-1) == SHAPE
+    assert call_step(d_in=-8) == SHAPE
+    assert call_step(d_out=-8) == SHAPE
+    assert call_step(d_in=12) == UNSUP
+    assert call_step(d_out=260) == UNSUP
+    assert call_step(d_in=1 << 16, d_out=1 << 16) == UNSUP          # 2^32 elements
+
+
+def test_empty_matrix_is_a_noop():
+    assert call_step(d_in=0, X=0, dY=0, W=0, m=0, v=0) == OK
+    assert call_step(d_out=0, X=0, dY=0, W=0, m=0, v=0) == OK
+    assert lib().forge_wgrad(0, 0, 0, 5, 0, 8, 0, None) == OK
+
+
+def test_null_pointer_errors():
+    assert call_step(W=0) == NULLP
+    assert call_step(m=0) == NULLP
+    assert call_step(v=0) == NULLP
+    assert call_step(X=0) == NULLP
+    assert call_step(dY=0) == NULLP
+    assert call_step(md=I8, ms=0) == NULLP
+    assert call_step(md=I8, vs=0) == NULLP
+    assert call_unfused(G=0) == NULLP
+    assert lib().forge_wgrad(BASE["X"], BASE["dY"], 0, 8, 8, 8, 0, None) == NULLP
+    assert lib().forge_adamw(0, 0, BASE["W"], BASE["m"], BASE["v"], 0, 0, 8, 8, BF16, 1e-3, 0.9, 0.999,
+                             1e-8, 0.1, 1, None) == NULLP
+
+
+def test_hyperparameter_errors():
+    assert call_step(step=0) == HYPER
+    assert call_step(step=-3) == HYPER
+    assert call_step(beta1=1.0) == HYPER
+    assert call_step(beta2=-0.1) == HYPER
+    assert call_step(eps=0.0) == HYPER
+    assert call_step(lr=-1e-3) == HYPER
+    assert call_step(lr=float("nan")) == HYPER
+    assert call_step(wd=float("inf")) == HYPER
+
+
+def test_alignment_errors():
+    assert call_step(W=BASE["W"] + 2) == MISAL
+    assert call_step(X=BASE["X"] + 8) == MISAL
+    assert call_step(md=I8, ms=BASE["ms"] + 4) == MISAL
+    assert call_unfused(G=BASE["G"] + 2) == MISAL
+
+
+def test_aliasing_errors():
+    P = 128 * 256
+    assert call_step(m=BASE["W"] + 16) == ALIAS                  # m overlaps W
+    assert call_step(v=BASE["m"] + 2 * P - 16) == ALIAS          # v starts inside m (bf16 m)
+    assert call_step(W=BASE["X"]) == ALIAS                       # output overlaps an input
+    assert call_step(W=BASE["dY"] + 16) == ALIAS
+    assert call_step(md=I8, vs=BASE["ms"]) == ALIAS
+    assert call_unfused(G=BASE["W"]) == ALIAS
+    assert call_unfused(G=BASE["X"]) == ALIAS
+    # adjacent, non-overlapping buffers are fine up to the device check
+    if not _gpu_visible():
+        assert call_step(m=BASE["W"] + 2 * P) == NODEV
+
+
+def _gpu_visible():
+    try:
+        import torch
+        return torch.cuda.is_available()
+    except Exception:
+        return False
+
+
+@pytest.mark.skipif(_gpu_visible(), reason="on a GPU machine a valid call would launch on fake pointers")
+def test_valid_arguments_reach_the_device_check():
+    assert call_step() == NODEV
+    assert call_step(T=0, X=0, dY=0) == NODEV
+
+
+def test_paper_bytes_per_parameter():
+    """Sec. 2.2: a standard bf16 step streams 16 B/param (gradient, both moments and the
+    weight, each written once and read once); the fused step moves 12."""
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "bytes_per_param.json")))
+    T, d = 0, 4096
+    P = d * d
+    assert accounting.fused_bytes(T, d, d, "bf16") / P == g["fused_bf16"]
+    assert accounting.unfused_bytes(T, d, d, "bf16", "bf16") / P == g["standard_bf16"]
+    assert g["standard_bf16"] / g["fused_bf16"] == pytest.approx(g["memory_bound_speedup_bound"], abs=0.005)  # printed to 2 decimals
