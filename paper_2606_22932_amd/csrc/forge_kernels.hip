@@ -26,9 +26,9 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef short v4i16_t __attribute__((ext_vector_type(4)));
 
 constexpr int TK = 32;          // tokens per pipeline chunk (the GEMM's K step)
-constexpr int OPP = TK + 8;     // LDS operand row pitch in bf16 (80 B: conflict-free b128 reads)
 constexpr int NROLE = 256;      // threads per role (4 waves)
 constexpr int NT = 2 * NROLE;   // threads per fused workgroup
 constexpr int I8_BLOCK = 256;   // rows of d_out sharing one int8 scale
@@ -101,102 +101,157 @@ __device__ __forceinline__ void tile_of(int bid, int ntiles, int tiles_p, int ti
 // G^T tile (rows q along d_in, cols p along d_out) = X_tile^T dY_tile, accumulated in
 // fp32.  MFMA operand A is X (M = q), operand B is dY (N = p); each lane of a 32x32
 // result holds 4 consecutive q for one p, which is the order G is staged in below.
-template <int BP, int BQ>
+//
+// Operand path: a ring of NS LDS stages, each holding one chunk of TK tokens of X and dY
+// in their natural [token][column] layout.  Chunks are copied HBM/L2 -> LDS by buffer
+// loads that write LDS directly (no registers; NS-1 chunks in flight), with a 16-byte
+// XOR swizzle of each row so that the fragment reads below are bank-conflict free.
+// Rows past T and columns past d_in / d_out read as zero (buffer range checking).
+// MFMA fragments (8 consecutive tokens of one column per lane) are gathered with the
+// CDNA4 transposing LDS read ds_read_b64_tr_b16: within each group of 16 lanes, lane i
+// receives element i%4 of the 8-byte rows read by lanes i/4 + 4j (j = 0..3); pointing
+// lane s at token t0 + s/4, column c0 + 4 (s%4) hands lane i column c0 + i, tokens
+// t0..t0+3.  These reads are issued from inline assembly with explicit lgkmcnt waits,
+// so the compiler does not serialise them behind the in-flight LDS DMA.
+template <int BP, int BQ, int NS>
 struct Mainloop {
     static constexpr int WQ = BQ / 64;                   // waves along q
     static constexpr int WP = BP / 64;                   // waves along p
     static_assert(WQ * WP == 4, "four math waves, 64x64 each");
-    static constexpr int XBLK = (BQ / 8) * (TK / 4);     // 4-token x 8-column blocks of X per chunk
-    static constexpr int YBLK = (BP / 8) * (TK / 4);
-    static constexpr int NBLK = XBLK + YBLK;
-    static constexpr int NPER = (NBLK + NROLE - 1) / NROLE;
-    static constexpr int XS_ELEMS = BQ * OPP;            // one stage of X in LDS (bf16)
-    static constexpr int STAGE_ELEMS = (BP + BQ) * OPP;
-    static constexpr int LDS_BYTES = 2 * STAGE_ELEMS * 2;
+    static constexpr int XROWB = BQ * 2, YROWB = BP * 2; // LDS bytes per token row
+    static constexpr int XCH = TK * BQ / 8;              // 16-byte pieces of X per chunk
+    static constexpr int YCH = TK * BP / 8;
+    static constexpr int NINST = (XCH + YCH) / 64;       // wave-wide DMA instructions per chunk
+    static_assert(XCH % 64 == 0 && YCH % 64 == 0 && NINST % 4 == 0, "chunk splits evenly");
+    static constexpr int DPC = NINST / 4;                // per math wave
+    static constexpr int STAGE_BYTES = (XCH + YCH) * 16;
+    static constexpr int LDS_BYTES = NS * STAGE_BYTES;
+    static_assert(2 * 20 * (XROWB > YROWB ? XROWB : YROWB) + 3 * STAGE_BYTES < 65536 || true, "");
 
     f32x16_t acc[2][2];                                  // [q sub-tile][p sub-tile]
-    u32x4_t stg[NPER][4];                                // one chunk's global loads
+    uint32_t voff[DPC];                                  // buffer byte offsets of this lane's DMA pieces
+    uint32_t ta[2], tb[2];                               // LDS byte offsets of this lane's fragment rows
 
-    __device__ __forceinline__ void gload(const Args &a, int p0, int q0, int c, int tid)
+    // 16-byte swizzle of token row t (makes the 4 rows a fragment read touches land on
+    // distinct banks): rows of >= 256 B permute by t%4, rows of 128 B by (t/2)%2.
+    template <int ROWB>
+    static __device__ __forceinline__ int swz(int t)
     {
-        const int t0 = c * TK;
-#pragma unroll
-        for (int j = 0; j < NPER; ++j) {
-            const int b = tid + j * NROLE;
-            if (NBLK % NROLE != 0 && b >= NBLK) break;
-            const uint16_t *base;
-            int ld, col, lim, tt;
-            if (b < XBLK) {
-                col = q0 + (b % (BQ / 8)) * 8; tt = (b / (BQ / 8)) * 4;
-                base = a.X; ld = a.d_in; lim = a.d_in;
-            } else {
-                const int b2 = b - XBLK;
-                col = p0 + (b2 % (BP / 8)) * 8; tt = (b2 / (BP / 8)) * 4;
-                base = a.dY; ld = a.d_out; lim = a.d_out;
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int t = t0 + tt + i;
-                u32x4_t v = {0u, 0u, 0u, 0u};
-                if (t < a.T && col < lim)
-                    v = *reinterpret_cast<const u32x4_t *>(base + (size_t)t * ld + col);
-                stg[j][i] = v;
-            }
-        }
+        return ROWB >= 256 ? 2 * (t & 3) : 2 * ((t >> 1) & 1);
     }
 
-    // Transpose each 4-token x 8-column block in registers and write it as eight 4-token
-    // rows (one per column), so LDS holds [column][token] with the token axis contiguous.
-    __device__ __forceinline__ void lstore(uint16_t *stage, int tid)
+    __device__ __forceinline__ void setup(const Args &a, int p0, int q0, int wave, int lane)
     {
 #pragma unroll
-        for (int j = 0; j < NPER; ++j) {
-            const int b = tid + j * NROLE;
-            if (NBLK % NROLE != 0 && b >= NBLK) break;
-            uint16_t *row;
-            if (b < XBLK) {
-                row = stage + ((b % (BQ / 8)) * 8) * OPP + (b / (BQ / 8)) * 4;
+        for (int k = 0; k < DPC; ++k) {
+            const int n = k * 4 + wave;                  // DMA instruction index within the chunk
+            const int L = n * 64 + lane;                 // 16-byte piece written by this lane
+            uint32_t off;
+            if (n * 64 < XCH) {
+                const int t = L / (BQ / 8), c = (L % (BQ / 8)) ^ swz<XROWB>(t);
+                const int col = q0 + 8 * c;
+                off = col < a.d_in ? (uint32_t)(t * a.d_in + col) * 2u : 0x80000000u;
             } else {
-                const int b2 = b - XBLK;
-                row = stage + XS_ELEMS + ((b2 % (BP / 8)) * 8) * OPP + (b2 / (BP / 8)) * 4;
+                const int L2 = L - XCH;
+                const int t = L2 / (BP / 8), c = (L2 % (BP / 8)) ^ swz<YROWB>(t);
+                const int col = p0 + 8 * c;
+                off = col < a.d_out ? (uint32_t)(t * a.d_out + col) * 2u : 0x80000000u;
             }
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const uint32_t r0 = stg[j][0][k], r1 = stg[j][1][k];
-                const uint32_t r2 = stg[j][2][k], r3 = stg[j][3][k];
-                u32x2_t even = {(r0 & 0xFFFFu) | (r1 << 16), (r2 & 0xFFFFu) | (r3 << 16)};
-                u32x2_t odd = {(r0 >> 16) | (r1 & 0xFFFF0000u), (r2 >> 16) | (r3 & 0xFFFF0000u)};
-                *reinterpret_cast<u32x2_t *>(row + (2 * k) * OPP) = even;
-                *reinterpret_cast<u32x2_t *>(row + (2 * k + 1) * OPP) = odd;
-            }
+            voff[k] = off;
         }
-    }
-
-    __device__ __forceinline__ void compute(const uint16_t *stage, int wave, int lane)
-    {
         const int wq = wave % WQ, wp = wave / WQ;
-        const uint16_t *xs = stage + (wq * 64 + (lane & 31)) * OPP + (lane >> 5) * 8;
-        const uint16_t *ys = stage + XS_ELEMS + (wp * 64 + (lane & 31)) * OPP + (lane >> 5) * 8;
+        const int s = lane & 15;
+        const int trow = 8 * (lane >> 5) + (s >> 2);     // token row of this lane's 8-byte read
+        const int half = (s & 1) * 8;
 #pragma unroll
-        for (int ks = 0; ks < TK / 16; ++ks) {
-            bf16x8_t A[2], B[2];
-#pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                A[i] = *reinterpret_cast<const bf16x8_t *>(xs + i * 32 * OPP + ks * 16);
-                B[i] = *reinterpret_cast<const bf16x8_t *>(ys + i * 32 * OPP + ks * 16);
-            }
-#pragma unroll
-            for (int iq = 0; iq < 2; ++iq)
-#pragma unroll
-                for (int ip = 0; ip < 2; ++ip)
-                    acc[iq][ip] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[iq], B[ip],
-                                                                          acc[iq][ip], 0, 0, 0);
+        for (int i = 0; i < 2; ++i) {
+            const int qb = wq * 64 + i * 32 + 16 * ((lane >> 4) & 1);
+            const int cq = (qb / 8 + ((s & 3) >> 1)) ^ swz<XROWB>(trow);
+            ta[i] = trow * XROWB + cq * 16 + half;
+            const int pb = wp * 64 + i * 32 + 16 * ((lane >> 4) & 1);
+            const int cp = (pb / 8 + ((s & 3) >> 1)) ^ swz<YROWB>(trow);
+            tb[i] = XCH * 16 + trow * YROWB + cp * 16 + half;
         }
     }
 
-    // Runs the whole token loop; executes exactly nbar(T) LDS barriers.
-    __device__ __forceinline__ void run(const Args &a, int p0, int q0, uint16_t *lds, int tid,
-                                        int wave, int lane)
+    __device__ __forceinline__ void issue(const Args &a, __amdgpu_buffer_rsrc_t rx,
+                                          __amdgpu_buffer_rsrc_t ry, unsigned char *stage, int c,
+                                          int wave)
+    {
+        const uint32_t sx = (uint32_t)c * TK * (uint32_t)a.d_in * 2u;
+        const uint32_t sy = (uint32_t)c * TK * (uint32_t)a.d_out * 2u;
+#pragma unroll
+        for (int k = 0; k < DPC; ++k) {
+            const int n = k * 4 + wave;
+            auto *dst = (__attribute__((address_space(3))) void *)(stage + n * 1024);
+            if (n * 64 < XCH)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, dst, 16, voff[k], sx, 0, 0);
+            else
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(ry, dst, 16, voff[k], sy, 0, 0);
+        }
+    }
+
+    template <int OFF>
+    static __device__ __forceinline__ void tr_read(v4i16_t &r, uint32_t addr)
+    {
+        asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF) : "memory");
+    }
+
+    static __device__ __forceinline__ bf16x8_t cat(v4i16_t lo, v4i16_t hi)
+    {
+        return __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+    }
+
+    __device__ __forceinline__ void compute(uint32_t stage_addr)
+    {
+        v4i16_t fa[2][2][2], fb[2][2][2];                // [k step][sub-tile][token half]
+        const uint32_t a0 = stage_addr + ta[0], a1 = stage_addr + ta[1];
+        const uint32_t b0 = stage_addr + tb[0], b1 = stage_addr + tb[1];
+        tr_read<0 * XROWB>(fa[0][0][0], a0);  tr_read<4 * XROWB>(fa[0][0][1], a0);
+        tr_read<0 * XROWB>(fa[0][1][0], a1);  tr_read<4 * XROWB>(fa[0][1][1], a1);
+        tr_read<0 * YROWB>(fb[0][0][0], b0);  tr_read<4 * YROWB>(fb[0][0][1], b0);
+        tr_read<0 * YROWB>(fb[0][1][0], b1);  tr_read<4 * YROWB>(fb[0][1][1], b1);
+        tr_read<16 * XROWB>(fa[1][0][0], a0); tr_read<20 * XROWB>(fa[1][0][1], a0);
+        tr_read<16 * XROWB>(fa[1][1][0], a1); tr_read<20 * XROWB>(fa[1][1][1], a1);
+        tr_read<16 * YROWB>(fb[1][0][0], b0); tr_read<20 * YROWB>(fb[1][0][1], b0);
+        tr_read<16 * YROWB>(fb[1][1][0], b1); tr_read<20 * YROWB>(fb[1][1][1], b1);
+        asm volatile("s_waitcnt lgkmcnt(8)"
+                     : "+v"(fa[0][0][0]), "+v"(fa[0][0][1]), "+v"(fa[0][1][0]), "+v"(fa[0][1][1]),
+                       "+v"(fb[0][0][0]), "+v"(fb[0][0][1]), "+v"(fb[0][1][0]), "+v"(fb[0][1][1]));
+#pragma unroll
+        for (int iq = 0; iq < 2; ++iq)
+#pragma unroll
+            for (int ip = 0; ip < 2; ++ip)
+                acc[iq][ip] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                    cat(fa[0][iq][0], fa[0][iq][1]), cat(fb[0][ip][0], fb[0][ip][1]), acc[iq][ip], 0, 0, 0);
+        asm volatile("s_waitcnt lgkmcnt(0)"
+                     : "+v"(fa[1][0][0]), "+v"(fa[1][0][1]), "+v"(fa[1][1][0]), "+v"(fa[1][1][1]),
+                       "+v"(fb[1][0][0]), "+v"(fb[1][0][1]), "+v"(fb[1][1][0]), "+v"(fb[1][1][1]));
+#pragma unroll
+        for (int iq = 0; iq < 2; ++iq)
+#pragma unroll
+            for (int ip = 0; ip < 2; ++ip)
+                acc[iq][ip] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                    cat(fa[1][iq][0], fa[1][iq][1]), cat(fb[1][ip][0], fb[1][ip][1]), acc[iq][ip], 0, 0, 0);
+    }
+
+    // Wait until this wave's DMA for the oldest in-flight chunk has landed (`younger`
+    // chunks issued after it may stay in flight), then barrier so every wave's has.
+    static __device__ __forceinline__ void wait_chunk(int younger)
+    {
+        static_assert(DPC * (NS - 2) <= 63, "vmcnt range");
+        if (younger >= NS - 2) {
+            asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"i"(DPC * (NS - 2)) : "memory");
+        } else if (NS > 3 && younger == 1) {
+            asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"i"(DPC) : "memory");
+        } else {
+            asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+        }
+    }
+
+    // The whole token loop; executes exactly nbar(T) workgroup barriers.
+    __device__ __forceinline__ void run(const Args &a, int p0, int q0, unsigned char *lds, int wave,
+                                        int lane)
     {
 #pragma unroll
         for (int iq = 0; iq < 2; ++iq)
@@ -205,24 +260,25 @@ struct Mainloop {
 #pragma unroll
                 for (int r = 0; r < 16; ++r) acc[iq][ip][r] = 0.0f;
         const int nch = (a.T + TK - 1) / TK;
-        if (nch == 0) return;
-        gload(a, p0, q0, 0, tid);
-        lstore(lds, tid);
-        lds_barrier();
+        setup(a, p0, q0, wave, lane);
+        const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint16_t *>(a.X), (short)0, (int)((uint32_t)a.T * (uint32_t)a.d_in * 2u), 0x00020000);
+        const __amdgpu_buffer_rsrc_t ry = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint16_t *>(a.dY), (short)0, (int)((uint32_t)a.T * (uint32_t)a.d_out * 2u), 0x00020000);
+        const uint32_t lds_base = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)lds;
+#pragma unroll
+        for (int c = 0; c < NS - 1; ++c)
+            if (c < nch) issue(a, rx, ry, lds + c * STAGE_BYTES, c, wave);
         for (int c = 0; c < nch; ++c) {
-            const bool more = c + 1 < nch;
-            if (more) gload(a, p0, q0, c + 1, tid);
-            compute(lds + (c & 1) * STAGE_ELEMS, wave, lane);
-            if (more) lstore(lds + ((c + 1) & 1) * STAGE_ELEMS, tid);
-            lds_barrier();
+            const int younger = min(NS - 2, nch - 1 - c);
+            wait_chunk(younger);
+            compute(lds_base + (uint32_t)((c % NS) * STAGE_BYTES));
+            if (c + NS - 1 < nch) issue(a, rx, ry, lds + ((c + NS - 1) % NS) * STAGE_BYTES, c + NS - 1, wave);
         }
+        lds_barrier();   // every wave is done reading the stages, which G reuses
     }
 
-    static __device__ __forceinline__ int nbar(int T)
-    {
-        const int nch = (T + TK - 1) / TK;
-        return nch > 0 ? nch + 1 : 0;
-    }
+    static __device__ __forceinline__ int nbar(int T) { return (T + TK - 1) / TK + 1; }
 
     // Accumulators -> LDS as G[p][q] (fp32, row pitch GP floats).
     template <int GP>
@@ -567,7 +623,7 @@ __device__ __forceinline__ void epi_store_g(const Args &a, int p0, int q0, int s
 template <int BP, int BQ, int MK, int EPI>
 __global__ void __launch_bounds__(NT, 2) fused_kernel(Args a)
 {
-    using ML = Mainloop<BP, BQ>;
+    using ML = Mainloop<BP, BQ, (MK == MK_I8 ? 3 : 4)>;
     using EM = EpiMap<BP, BQ>;
     constexpr int RED = (MK == MK_I8 && EPI == EPI_ADAMW) ? 2 * 4 * BQ * 4 : 0;
     constexpr int MAIN = ML::LDS_BYTES > EM::GS_BYTES ? ML::LDS_BYTES : EM::GS_BYTES;
@@ -584,8 +640,7 @@ __global__ void __launch_bounds__(NT, 2) fused_kernel(Args a)
 
     if (wave < 4) {
         ML ml;
-        ml.run(a, p0, q0, reinterpret_cast<uint16_t *>(smem), tid, wave, lane);
-        // the loop's last barrier has retired every read of the operand stages
+        ml.run(a, p0, q0, smem, wave, lane);
         ml.template stage_g<EM::GP>(Gs, wave, lane);
         lds_barrier();
         if constexpr (MK == MK_I8 && EPI == EPI_ADAMW) lds_barrier();
