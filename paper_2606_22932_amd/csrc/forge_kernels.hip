@@ -32,6 +32,10 @@ constexpr int TK = 32;          // tokens per pipeline chunk (the GEMM's K step)
 constexpr int NROLE = 256;      // threads per role (4 waves)
 constexpr int NT = 2 * NROLE;   // threads per fused workgroup
 constexpr int I8_BLOCK = 256;   // rows of d_out sharing one int8 scale
+// Buffer offset of a DMA piece that must read zero.  Tensors hold fewer than 2^31
+// elements and d_in, d_out are multiples of 8, so a chunk spans at most 2^32 - 16 bytes:
+// this offset is past the end of every chunk's buffer.
+constexpr uint32_t OOR_OFFSET = 0xFFFFFFF0u;
 
 // Tile shapes: (rows along d_out) x (cols along d_in).  int8 tiles are exactly one scale
 // block tall so that the block absmax closes inside the workgroup.
@@ -146,18 +150,22 @@ struct Mainloop {
         for (int k = 0; k < DPC; ++k) {
             const int n = k * 4 + wave;                  // DMA instruction index within the chunk
             const int L = n * 64 + lane;                 // 16-byte piece written by this lane
-            uint32_t off;
+            // Byte offset within the chunk's buffer (its token rows only).  A piece past
+            // the last column, or one whose offset would not fit in 32 bits, gets
+            // OOR_OFFSET, which no chunk's record count reaches: it reads zero.
+            int t, col, ld;
             if (n * 64 < XCH) {
-                const int t = L / (BQ / 8), c = (L % (BQ / 8)) ^ swz<XROWB>(t);
-                const int col = q0 + 8 * c;
-                off = col < a.d_in ? (uint32_t)(t * a.d_in + col) * 2u : 0x80000000u;
+                t = L / (BQ / 8);
+                col = q0 + 8 * ((L % (BQ / 8)) ^ swz<XROWB>(t));
+                ld = a.d_in;
             } else {
                 const int L2 = L - XCH;
-                const int t = L2 / (BP / 8), c = (L2 % (BP / 8)) ^ swz<YROWB>(t);
-                const int col = p0 + 8 * c;
-                off = col < a.d_out ? (uint32_t)(t * a.d_out + col) * 2u : 0x80000000u;
+                t = L2 / (BP / 8);
+                col = p0 + 8 * ((L2 % (BP / 8)) ^ swz<YROWB>(t));
+                ld = a.d_out;
             }
-            voff[k] = off;
+            const uint64_t off = ((uint64_t)t * (uint64_t)ld + (uint64_t)col) * 2u;
+            voff[k] = (col < ld && off < OOR_OFFSET) ? (uint32_t)off : OOR_OFFSET;
         }
         const int wq = wave % WQ, wp = wave / WQ;
         const int s = lane & 15;
@@ -174,20 +182,27 @@ struct Mainloop {
         }
     }
 
-    __device__ __forceinline__ void issue(const Args &a, __amdgpu_buffer_rsrc_t rx,
-                                          __amdgpu_buffer_rsrc_t ry, unsigned char *stage, int c,
-                                          int wave)
+    // DMA of token chunk c into a stage.  Each chunk gets buffers of its own that start at
+    // its first token row and end at its last existing one, so rows past T read zero and
+    // no offset grows with the token position.
+    __device__ __forceinline__ void issue(const Args &a, unsigned char *stage, int c, int wave)
     {
-        const uint32_t sx = (uint32_t)c * TK * (uint32_t)a.d_in * 2u;
-        const uint32_t sy = (uint32_t)c * TK * (uint32_t)a.d_out * 2u;
+        const int rows = min(TK, a.T - c * TK);
+        const size_t r0 = (size_t)c * TK;
+        const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint16_t *>(a.X + r0 * (size_t)a.d_in), (short)0,
+            (int)((uint32_t)rows * (uint32_t)a.d_in * 2u), 0x00020000);
+        const __amdgpu_buffer_rsrc_t ry = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint16_t *>(a.dY + r0 * (size_t)a.d_out), (short)0,
+            (int)((uint32_t)rows * (uint32_t)a.d_out * 2u), 0x00020000);
 #pragma unroll
         for (int k = 0; k < DPC; ++k) {
             const int n = k * 4 + wave;
             auto *dst = (__attribute__((address_space(3))) void *)(stage + n * 1024);
             if (n * 64 < XCH)
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, dst, 16, voff[k], sx, 0, 0);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, dst, 16, voff[k], 0, 0, 0);
             else
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(ry, dst, 16, voff[k], sy, 0, 0);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(ry, dst, 16, voff[k], 0, 0, 0);
         }
     }
 
@@ -261,19 +276,15 @@ struct Mainloop {
                 for (int r = 0; r < 16; ++r) acc[iq][ip][r] = 0.0f;
         const int nch = (a.T + TK - 1) / TK;
         setup(a, p0, q0, wave, lane);
-        const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
-            const_cast<uint16_t *>(a.X), (short)0, (int)((uint32_t)a.T * (uint32_t)a.d_in * 2u), 0x00020000);
-        const __amdgpu_buffer_rsrc_t ry = __builtin_amdgcn_make_buffer_rsrc(
-            const_cast<uint16_t *>(a.dY), (short)0, (int)((uint32_t)a.T * (uint32_t)a.d_out * 2u), 0x00020000);
         const uint32_t lds_base = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)lds;
 #pragma unroll
         for (int c = 0; c < NS - 1; ++c)
-            if (c < nch) issue(a, rx, ry, lds + c * STAGE_BYTES, c, wave);
+            if (c < nch) issue(a, lds + c * STAGE_BYTES, c, wave);
         for (int c = 0; c < nch; ++c) {
             const int younger = min(NS - 2, nch - 1 - c);
             wait_chunk(younger);
             compute(lds_base + (uint32_t)((c % NS) * STAGE_BYTES));
-            if (c + NS - 1 < nch) issue(a, rx, ry, lds + ((c + NS - 1) % NS) * STAGE_BYTES, c + NS - 1, wave);
+            if (c + NS - 1 < nch) issue(a, lds + ((c + NS - 1) % NS) * STAGE_BYTES, c + NS - 1, wave);
         }
         lds_barrier();   // every wave is done reading the stages, which G reuses
     }
