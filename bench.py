@@ -29,7 +29,16 @@ COPY_BYTES = 1 << 30           # size of the calibration copy (--copy-calibratio
 # --no-unfused --copy-calibration` (FETCH_SIZE, then WRITE_SIZE), each counter scaled by
 # COPY_BYTES / (what it reads for the calibration copy).  Valid only for the kernel
 # source whose sha256 is recorded: after any change to it the figure is reported as null.
-TRAFFIC = {}
+TRAFFIC = {
+    "sweep": {
+        "source_sha256": "f8c737b6e94fd91dd52cf85a2ace6472167e4f4c2d6f767584d3daceea28042c",
+        "fetch_kib_per_launch": 120316.1,     # FETCH_SIZE, mean over the 225 launches
+        "write_kib_per_launch": 195454.6,     # WRITE_SIZE
+        "fetch_scale": 1.99995,               # 1 GiB copy: FETCH_SIZE reads 524302 KiB
+        "write_scale": 1.0,                   # 1 GiB copy: WRITE_SIZE reads 1048576 KiB
+        "bytes_per_launch": 446546218,        # (fetch * fetch_scale + write * write_scale) KiB
+    },
+}
 
 
 def log(*a):
@@ -55,31 +64,31 @@ def build_workload(wl, device, moment_override=None):
 
 
 def time_steps(mats, wl, fn, steps, warmup, step0):
-    """Run `warmup` untimed steps, then `steps` timed steps.  Returns (total ms, per-launch ms list)."""
+    """Run `warmup` untimed steps, then `steps` timed steps back to back on the current
+    stream (the one the library launches on), bracketed by two HIP events on that stream.
+
+    No event sits between launches: an event record between two kernels costs a gap of
+    about 5 us on this stream, while back-to-back launches follow each other with none, so
+    the region's time divided by its launches is the average kernel duration.
+    Returns (region ms, wall ms).
+    """
     import torch
     for i in range(warmup):
         for d in mats:
             fn(d, step0 + i)
-    torch.cuda.synchronize()
-    n = len(mats)
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n + 1)] for _ in range(steps)]
+    stream = torch.cuda.current_stream()
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    start.record()
+    start.record(stream)
     for s in range(steps):
-        e = evs[s]
-        e[0].record()
-        for j, d in enumerate(mats):
+        for d in mats:
             fn(d, step0 + warmup + s)
-            e[j + 1].record()
-    end.record()
+    end.record(stream)
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) * 1e3
-    total = start.elapsed_time(end)
-    per_launch = [[evs[s][j].elapsed_time(evs[s][j + 1]) for j in range(n)] for s in range(steps)]
-    return total, per_launch, wall
+    return start.elapsed_time(end), wall
 
 
 def source_sha256() -> str:
@@ -189,11 +198,10 @@ def main():
     fused_b = sum(accounting.fused_bytes(T, d["mat"].d_in, d["mat"].d_out, wl.moment) for d in mats)
     flops = sum(accounting.gemm_flops(T, d["mat"].d_in, d["mat"].d_out) for d in mats)
     log("timing fused")
-    total, per_launch, wall = time_steps(mats, wl, fused, args.steps, args.warmup, wl.steps[0])
+    total, wall = time_steps(mats, wl, fused, args.steps, args.warmup, wl.steps[0])
     ms = total / args.steps
-    launches = [x for s in per_launch for x in s]
-    avg_launch_ms = sum(launches) / len(launches)
-    kern_gbs = fused_b * args.steps / (sum(launches) * 1e-3) / 1e9
+    avg_launch_ms = total / (args.steps * len(mats))
+    kern_gbs = (fused_b / len(mats)) / (avg_launch_ms * 1e-3) / 1e9
     value = fused_b / (ms * 1e-3) / 1e9
     log(f"fused: {ms:.3f} ms/step, {value:.1f} GB/s, kernel-time {kern_gbs:.1f} GB/s, "
         f"MFMA {flops / (ms * 1e-3) / 1e12:.1f} TF/s, wall {wall:.1f} ms")
@@ -247,7 +255,7 @@ def main():
                                             G_ws=G_ws, step=t, **hp)
 
         log("timing unfused (GEMM stores bf16 G, then the optimizer kernel)")
-        ut, _, _ = time_steps(mats, wl, unfused, args.steps, args.warmup, wl.steps[0] + 1000)
+        ut, _ = time_steps(mats, wl, unfused, args.steps, args.warmup, wl.steps[0] + 1000)
         ums = ut / args.steps
         ub = sum(accounting.unfused_bytes(T, d["mat"].d_in, d["mat"].d_out, wl.moment, "bf16") for d in mats)
         out["unfused"] = {"ms_per_step": round(ums, 4), "algorithmic_bytes_per_step": ub,
