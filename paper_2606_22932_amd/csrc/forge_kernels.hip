@@ -28,7 +28,14 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 typedef short v4i16_t __attribute__((ext_vector_type(4)));
 
-constexpr int TK = 32;          // tokens per pipeline chunk (the GEMM's K step)
+#ifndef FORGE_TK
+#define FORGE_TK 32
+#endif
+#ifndef FORGE_NS
+#define FORGE_NS 4
+#endif
+constexpr int TK128 = FORGE_TK;   // tokens per pipeline chunk (the GEMM's K step), 128x128 tiles
+constexpr int NSTAGE = FORGE_NS;  // LDS ring depth (chunks) of the 128x128 mainloop
 constexpr int NROLE = 256;      // threads per role (4 waves)
 constexpr int NT = 2 * NROLE;   // threads per fused workgroup
 constexpr int I8_BLOCK = 256;   // rows of d_out sharing one int8 scale
@@ -117,12 +124,14 @@ __device__ __forceinline__ void tile_of(int bid, int ntiles, int tiles_p, int ti
 // lane s at token t0 + s/4, column c0 + 4 (s%4) hands lane i column c0 + i, tokens
 // t0..t0+3.  These reads are issued from inline assembly with explicit lgkmcnt waits,
 // so the compiler does not serialise them behind the in-flight LDS DMA.
-template <int BP, int BQ, int NS>
+template <int BP, int BQ, int NS, int TK = 32>
 struct Mainloop {
+    static_assert(TK % 32 == 0, "chunks are whole pairs of 16-token MFMA steps");
     static constexpr int WQ = BQ / 64;                   // waves along q
     static constexpr int WP = BP / 64;                   // waves along p
     static_assert(WQ * WP == 4, "four math waves, 64x64 each");
     static constexpr int XROWB = BQ * 2, YROWB = BP * 2; // LDS bytes per token row
+    static_assert(TK == 32 || XROWB == YROWB, "a stage of several 32-token steps needs equal row lengths");
     static constexpr int XCH = TK * BQ / 8;              // 16-byte pieces of X per chunk
     static constexpr int YCH = TK * BP / 8;
     static constexpr int NINST = (XCH + YCH) / 64;       // wave-wide DMA instructions per chunk
@@ -136,12 +145,16 @@ struct Mainloop {
     uint32_t voff[DPC];                                  // buffer byte offsets of this lane's DMA pieces
     uint32_t ta[2], tb[2];                               // LDS byte offsets of this lane's fragment rows
 
-    // 16-byte swizzle of token row t (makes the 4 rows a fragment read touches land on
-    // distinct banks): rows of >= 256 B permute by t%4, rows of 128 B by (t/2)%2.
+    // 16-byte swizzle of token row t.  Half a wave's transposing read covers 4 token rows
+    // x 4 aligned 16-byte pieces (64 B per row); the LDS serves 256 B (64 banks) per cycle.
+    // XOR-ing the piece index with a multiple of 4 moves each row's 64 B to its own quarter
+    // of the banks: rows of >= 256 B use 4*(t%4), rows of 128 B (two rows per bank sweep)
+    // use 4*((t/2)%2).  Without it the 4 rows collide two by two.
     template <int ROWB>
     static __device__ __forceinline__ int swz(int t)
     {
-        return ROWB >= 256 ? 2 * (t & 3) : 2 * ((t >> 1) & 1);
+        static_assert(ROWB >= 128, "at least 8 pieces per row");
+        return ROWB >= 256 ? 4 * (t & 3) : 4 * ((t >> 1) & 1);
     }
 
     __device__ __forceinline__ void setup(const Args &a, int p0, int q0, int wave, int lane)
@@ -283,7 +296,9 @@ struct Mainloop {
         for (int c = 0; c < nch; ++c) {
             const int younger = min(NS - 2, nch - 1 - c);
             wait_chunk(younger);
-            compute(lds_base + (uint32_t)((c % NS) * STAGE_BYTES));
+#pragma unroll
+            for (int h = 0; h < TK / 32; ++h)    // 32 tokens per compute(); X and Y rows of equal length
+                compute(lds_base + (uint32_t)((c % NS) * STAGE_BYTES + h * 32 * XROWB));
             if (c + NS - 1 < nch) issue(a, lds + ((c + NS - 1) % NS) * STAGE_BYTES, c + NS - 1, wave);
         }
         lds_barrier();   // every wave is done reading the stages, which G reuses
@@ -333,22 +348,28 @@ struct EpiAdamW {
     static constexpr bool PREFETCH = (MK == MK_BF16);   // fp32 state would not fit in registers
     u32x4_t pw[PREFETCH ? M::NPASS : 1], pm[PREFETCH ? M::NPASS : 1], pv[PREFETCH ? M::NPASS : 1];
 
-    __device__ __forceinline__ void prefetch(const Args &a, int p0, int q0, int s)
+    // Loads of pass I (one row per lane) into the prefetch registers.
+    template <int I>
+    __device__ __forceinline__ void prefetch_pass(const Args &a, int p0, int q0, int s)
     {
         if constexpr (PREFETCH) {
             const int rs = s / M::LPR, q = q0 + (s % M::LPR) * 8;
-#pragma unroll
-            for (int i = 0; i < M::NPASS; ++i) {
-                const int p = p0 + i * M::RPP + rs;
-                pw[i] = pm[i] = pv[i] = u32x4_t{0u, 0u, 0u, 0u};
-                if (q < a.d_in && p < a.d_out) {
-                    const size_t off = (size_t)p * a.d_in + q;
-                    pw[i] = ld_nt<u32x4_t>(a.W + off);
-                    pm[i] = ld_nt<u32x4_t>(static_cast<const uint16_t *>(a.m) + off);
-                    pv[i] = ld_nt<u32x4_t>(static_cast<const uint16_t *>(a.v) + off);
-                }
+            const int p = p0 + I * M::RPP + rs;
+            pw[I] = pm[I] = pv[I] = u32x4_t{0u, 0u, 0u, 0u};
+            if (q < a.d_in && p < a.d_out) {
+                const size_t off = (size_t)p * a.d_in + q;
+                pw[I] = ld_nt<u32x4_t>(a.W + off);
+                pm[I] = ld_nt<u32x4_t>(static_cast<const uint16_t *>(a.m) + off);
+                pv[I] = ld_nt<u32x4_t>(static_cast<const uint16_t *>(a.v) + off);
             }
         }
+    }
+
+    template <int I = 0>
+    __device__ __forceinline__ void prefetch(const Args &a, int p0, int q0, int s)
+    {
+        prefetch_pass<I>(a, p0, q0, s);
+        if constexpr (I + 1 < M::NPASS) prefetch<I + 1>(a, p0, q0, s);
     }
 
     __device__ __forceinline__ void run(const Args &a, int p0, int q0, int s, const float *Gs)
@@ -634,7 +655,7 @@ __device__ __forceinline__ void epi_store_g(const Args &a, int p0, int q0, int s
 template <int BP, int BQ, int MK, int EPI>
 __global__ void __launch_bounds__(NT, 2) fused_kernel(Args a)
 {
-    using ML = Mainloop<BP, BQ, (MK == MK_I8 ? 3 : 4)>;
+    using ML = Mainloop<BP, BQ, (MK == MK_I8 ? 3 : NSTAGE), (MK == MK_I8 ? 32 : TK128)>;
     using EM = EpiMap<BP, BQ>;
     constexpr int RED = (MK == MK_I8 && EPI == EPI_ADAMW) ? 2 * 4 * BQ * 4 : 0;
     constexpr int MAIN = ML::LDS_BYTES > EM::GS_BYTES ? ML::LDS_BYTES : EM::GS_BYTES;
@@ -645,45 +666,40 @@ __global__ void __launch_bounds__(NT, 2) fused_kernel(Args a)
     const int tid = threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int lane = tid & 63;
-    int tp, tq;
-    tile_of(blockIdx.x, gridDim.x, a.tiles_p, a.tiles_q, a.group_p, tp, tq);
-    const int p0 = tp * BP, q0 = tq * BQ;
-
-    if (wave < 4) {
-        ML ml;
-        ml.run(a, p0, q0, smem, wave, lane);
-        ml.template stage_g<EM::GP>(Gs, wave, lane);
-        lds_barrier();
-        if constexpr (MK == MK_I8 && EPI == EPI_ADAMW) lds_barrier();
-        return;
-    }
-
     const int s = tid - NROLE;
     const int nbar = ML::nbar(a.T);
-    if constexpr (EPI == EPI_ADAMW) {
-        if constexpr (MK == MK_I8) {
-            EpiAdamWI8<BP, BQ> ep;
-            ep.prefetch(a, p0, q0, s);
-            for (int i = 0; i < nbar; ++i) lds_barrier();
+    {
+        int tp, tq;
+        tile_of(blockIdx.x, a.tiles_p * a.tiles_q, a.tiles_p, a.tiles_q, a.group_p, tp, tq);
+        const int p0 = tp * BP, q0 = tq * BQ;
+        if (wave < 4) {
+            ML ml;
+            ml.run(a, p0, q0, smem, wave, lane);
+            ml.template stage_g<EM::GP>(Gs, wave, lane);
             lds_barrier();
-            ep.run(a, p0, q0, s, Gs, red);
+            if constexpr (MK == MK_I8 && EPI == EPI_ADAMW) lds_barrier();
+        } else if constexpr (EPI == EPI_ADAMW) {
+            if constexpr (MK == MK_I8) {
+                EpiAdamWI8<BP, BQ> ep;
+                ep.prefetch(a, p0, q0, s);
+                for (int i = 0; i < nbar; ++i) lds_barrier();
+                lds_barrier();
+                ep.run(a, p0, q0, s, Gs, red);
+            } else {
+                EpiAdamW<BP, BQ, MK> ep;
+                ep.prefetch(a, p0, q0, s);
+                for (int i = 0; i < nbar; ++i) lds_barrier();
+                lds_barrier();
+                ep.run(a, p0, q0, s, Gs);
+            }
         } else {
-            EpiAdamW<BP, BQ, MK> ep;
-            ep.prefetch(a, p0, q0, s);
             for (int i = 0; i < nbar; ++i) lds_barrier();
             lds_barrier();
-            ep.run(a, p0, q0, s, Gs);
+            epi_store_g<BP, BQ, EPI == EPI_STORE_F32>(a, p0, q0, s, Gs);
         }
-    } else {
-        for (int i = 0; i < nbar; ++i) lds_barrier();
-        lds_barrier();
-        epi_store_g<BP, BQ, EPI == EPI_STORE_F32>(a, p0, q0, s, Gs);
     }
 }
 
-// Stand-alone optimizer over a materialised gradient: 256 threads per tile; each thread
-// prefetches its state, the tile of G is staged into LDS (fp32), then the same epilogue
-// as the fused kernel runs.
 template <int BP, int BQ, int MK, bool GF32>
 __global__ void __launch_bounds__(NROLE, 2) adamw_kernel(Args a)
 {
@@ -738,8 +754,8 @@ __global__ void __launch_bounds__(NROLE, 2) adamw_kernel(Args a)
 
 TileShape tile_shape(int mk)
 {
-    if (mk == MK_I8) return TileShape{BP_I8, BQ_I8, TK};
-    return TileShape{BP_F, BQ_F, TK};
+    if (mk == MK_I8) return TileShape{BP_I8, BQ_I8, 32};
+    return TileShape{BP_F, BQ_F, TK128};
 }
 
 static Args with_grid(Args a, int bp, int bq, int &ntiles)
