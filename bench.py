@@ -63,7 +63,7 @@ def build_workload(wl, device, moment_override=None):
     return mats
 
 
-def time_steps(mats, wl, fn, steps, warmup, step0):
+def time_steps(launches, wl, fn, steps, warmup, step0):
     """Run `warmup` untimed steps, then `steps` timed steps back to back on the current
     stream (the one the library launches on), bracketed by two HIP events on that stream.
 
@@ -74,8 +74,8 @@ def time_steps(mats, wl, fn, steps, warmup, step0):
     """
     import torch
     for i in range(warmup):
-        for d in mats:
-            fn(d, step0 + i)
+        for unit in launches:
+            fn(unit, step0 + i)
     stream = torch.cuda.current_stream()
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
@@ -83,8 +83,8 @@ def time_steps(mats, wl, fn, steps, warmup, step0):
     t0 = time.perf_counter()
     start.record(stream)
     for s in range(steps):
-        for d in mats:
-            fn(d, step0 + warmup + s)
+        for unit in launches:
+            fn(unit, step0 + warmup + s)
     end.record(stream)
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) * 1e3
@@ -192,16 +192,21 @@ def main():
     hp = wl.hyper
     T = wl.T
 
-    def fused(d, t):
-        forge.forge_linear_step(d["X"], d["dY"], d["W"], d["m"], d["v"], d["ms"], d["vs"], step=t, **hp)
+    # One fused launch per group of matrices whose gradients a backward pass makes available
+    # together (one matrix per launch except q/k/v and gate/up of the sweep).
+    launches = [[mats[i] for i in g] for g in synth.launch_groups(wl)]
+
+    def fused(group, t):
+        forge.forge_linear_step_grouped([(d["X"], d["dY"], d["W"], d["m"], d["v"], d["ms"], d["vs"])
+                                         for d in group], step=t, **hp)
 
     fused_b = sum(accounting.fused_bytes(T, d["mat"].d_in, d["mat"].d_out, wl.moment) for d in mats)
     flops = sum(accounting.gemm_flops(T, d["mat"].d_in, d["mat"].d_out) for d in mats)
-    log("timing fused")
-    total, wall = time_steps(mats, wl, fused, args.steps, args.warmup, wl.steps[0])
+    log(f"timing fused ({len(launches)} launches per step)")
+    total, wall = time_steps(launches, wl, fused, args.steps, args.warmup, wl.steps[0])
     ms = total / args.steps
-    avg_launch_ms = total / (args.steps * len(mats))
-    kern_gbs = (fused_b / len(mats)) / (avg_launch_ms * 1e-3) / 1e9
+    avg_launch_ms = total / (args.steps * len(launches))
+    kern_gbs = (fused_b / len(launches)) / (avg_launch_ms * 1e-3) / 1e9
     value = fused_b / (ms * 1e-3) / 1e9
     log(f"fused: {ms:.3f} ms/step, {value:.1f} GB/s, kernel-time {kern_gbs:.1f} GB/s, "
         f"MFMA {flops / (ms * 1e-3) / 1e12:.1f} TF/s, wall {wall:.1f} ms")
@@ -237,10 +242,10 @@ def main():
             "unit": "GB/s",
             "frac": round(kern_gbs / HBM_PEAK_GBS, 4),
             "traffic": traffic,
-            "kernel": "fused_kernel (forge_linear_step)",
-            "algorithmic_bytes_per_launch": round(fused_b / len(mats)),
+            "kernel": "fused_kernel (forge_linear_step_grouped)",
+            "algorithmic_bytes_per_launch": round(fused_b / len(launches)),
             "avg_launch_us": round(avg_launch_ms * 1e3, 3),
-            "launches_per_step": len(mats),
+            "launches_per_step": len(launches),
         },
         "mfma_tflops": round(flops / (ms * 1e-3) / 1e12, 2),
         "mfma_frac": round(flops / (ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFS, 4),
@@ -250,12 +255,13 @@ def main():
         biggest = max(d["mat"].d_in * d["mat"].d_out for d in mats)
         G_ws = torch.empty(biggest, dtype=torch.bfloat16, device=device)
 
-        def unfused(d, t):
-            forge.forge_linear_step_unfused(d["X"], d["dY"], d["W"], d["m"], d["v"], d["ms"], d["vs"],
-                                            G_ws=G_ws, step=t, **hp)
+        def unfused(group, t):
+            for d in group:
+                forge.forge_linear_step_unfused(d["X"], d["dY"], d["W"], d["m"], d["v"], d["ms"], d["vs"],
+                                                G_ws=G_ws, step=t, **hp)
 
         log("timing unfused (GEMM stores bf16 G, then the optimizer kernel)")
-        ut, _ = time_steps(mats, wl, unfused, args.steps, args.warmup, wl.steps[0] + 1000)
+        ut, _ = time_steps([[d] for d in mats], wl, unfused, args.steps, args.warmup, wl.steps[0] + 1000)
         ums = ut / args.steps
         ub = sum(accounting.unfused_bytes(T, d["mat"].d_in, d["mat"].d_out, wl.moment, "bf16") for d in mats)
         out["unfused"] = {"ms_per_step": round(ums, 4), "algorithmic_bytes_per_step": ub,

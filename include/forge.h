@@ -38,6 +38,14 @@
 
 #include <stdint.h>
 
+/* Entry points are the library's only exported symbols (it is built with hidden default
+   visibility). */
+#if defined(__GNUC__) || defined(__clang__)
+#define FORGE_API __attribute__((visibility("default")))
+#else
+#define FORGE_API
+#endif
+
 #ifdef __cplusplus
 extern "C" {
 #endif
@@ -85,18 +93,57 @@ typedef enum {
  * The gradient is accumulated in fp32 from bf16 products; the update runs in fp32; W is
  * stored to bf16 with round-to-nearest-even.  No gradient byte is written to memory.
  */
-forge_status forge_linear_step(const void *X, const void *dY, void *W, void *m, void *v,
+FORGE_API forge_status forge_linear_step(const void *X, const void *dY, void *W, void *m, void *v,
                                float *m_scale, float *v_scale, int64_t T, int64_t d_in,
                                int64_t d_out, int32_t moment_dtype, float lr, float beta1,
                                float beta2, float eps, float weight_decay, int64_t step,
                                void *stream);
+
+/* Upper bound on the matrices of one forge_linear_step_grouped call. */
+#define FORGE_MAX_GROUP 8
+
+/* One matrix of a grouped step: the per-matrix arguments of forge_linear_step. */
+typedef struct forge_matrix {
+    const void *X;            /* bf16 [T, d_in] (may be NULL when T == 0) */
+    const void *dY;           /* bf16 [T, d_out] (may be NULL when T == 0) */
+    void *W;                  /* bf16 [d_out, d_in], in/out */
+    void *m, *v;              /* [d_out, d_in] moments in the group's moment dtype, in/out */
+    float *m_scale, *v_scale; /* int8 only: fp32 [ceil(d_out/256), d_in], in/out */
+    int64_t d_in, d_out;
+} forge_matrix;
+
+/*
+ * forge_linear_step_grouped -- forge_linear_step on n independent matrices in one launch.
+ *
+ * The weight gradients of one layer's projections that share an input and become
+ * available together in the backward pass (for example q, k, v, or an MLP's gate and up)
+ * can be stepped by one launch: the tiles of all matrices form one grid, so the machine
+ * stays full across them.  Each matrix gets exactly the arithmetic of forge_linear_step
+ * (the result is bit-identical to n separate calls): Algorithm 1 is tile-local (App. A,
+ * Def. 1), so how tiles are grouped into launches does not change any value.
+ *
+ *   mats     host array of n descriptors, read during the call only (caller-owned)
+ *   n        1 <= n <= FORGE_MAX_GROUP, else FORGE_ERR_INVALID_SHAPE
+ *   T, moment_dtype, lr, beta1, beta2, eps, weight_decay, step, stream
+ *            shared by all matrices, as in forge_linear_step
+ *
+ * Validation, in this order: the moment dtype; mats (NULL: FORGE_ERR_NULL_POINTER) and n;
+ * each matrix in turn with forge_linear_step's shape, input-pointer and state-tensor rules;
+ * the hyper-parameters; aliasing -- the state tensors (W, m, v and the scales) of all
+ * matrices must be pairwise disjoint and disjoint from every matrix's X and dY
+ * (FORGE_ERR_ALIASING; matrices may share X or dY); the device.  Matrices with d_in or
+ * d_out == 0 are skipped; if all are empty the call returns FORGE_OK without a launch.
+ */
+FORGE_API forge_status forge_linear_step_grouped(const forge_matrix *mats, int32_t n, int64_t T,
+                                       int32_t moment_dtype, float lr, float beta1, float beta2,
+                                       float eps, float weight_decay, int64_t step, void *stream);
 
 /*
  * forge_wgrad -- the weight-gradient GEMM alone, storing G = dY^T X (Eq. wgrad) to
  * `G` [d_out, d_in] in `grad_dtype` (bf16 with round-to-nearest-even, or fp32).  This is
  * the first kernel of the two-kernel comparison path and the store-G control of App. D.
  */
-forge_status forge_wgrad(const void *X, const void *dY, void *G, int64_t T, int64_t d_in,
+FORGE_API forge_status forge_wgrad(const void *X, const void *dY, void *G, int64_t T, int64_t d_in,
                          int64_t d_out, int32_t grad_dtype, void *stream);
 
 /*
@@ -104,7 +151,7 @@ forge_status forge_wgrad(const void *X, const void *dY, void *G, int64_t T, int6
  * update then weight update) reading a materialised gradient `G` [d_out, d_in] in
  * `grad_dtype`.  Arguments as in forge_linear_step.  G is read only.
  */
-forge_status forge_adamw(const void *G, int32_t grad_dtype, void *W, void *m, void *v,
+FORGE_API forge_status forge_adamw(const void *G, int32_t grad_dtype, void *W, void *m, void *v,
                          float *m_scale, float *v_scale, int64_t d_in, int64_t d_out,
                          int32_t moment_dtype, float lr, float beta1, float beta2, float eps,
                          float weight_decay, int64_t step, void *stream);
@@ -117,7 +164,7 @@ forge_status forge_adamw(const void *G, int32_t grad_dtype, void *W, void *m, vo
  * write and read).  With a bf16 workspace the optimizer sees G rounded to bf16 (the
  * truncation discussed in App. B).
  */
-forge_status forge_linear_step_unfused(const void *X, const void *dY, void *W, void *m,
+FORGE_API forge_status forge_linear_step_unfused(const void *X, const void *dY, void *W, void *m,
                                        void *v, float *m_scale, float *v_scale, int64_t T,
                                        int64_t d_in, int64_t d_out, int32_t moment_dtype,
                                        float lr, float beta1, float beta2, float eps,
@@ -125,14 +172,14 @@ forge_status forge_linear_step_unfused(const void *X, const void *dY, void *W, v
                                        int32_t grad_dtype, void *stream);
 
 /* Static description of a status code (never NULL). */
-const char *forge_status_string(int32_t status);
+FORGE_API const char *forge_status_string(int32_t status);
 
 /*
  * forge_query_tile -- the tile geometry the fused kernel uses for `moment_dtype`:
  * rows of W (along d_out), columns (along d_in) and tokens per pipeline chunk.
  * Any output pointer may be NULL.  Returns FORGE_ERR_INVALID_DTYPE for an unknown code.
  */
-forge_status forge_query_tile(int32_t moment_dtype, int32_t *tile_rows, int32_t *tile_cols,
+FORGE_API forge_status forge_query_tile(int32_t moment_dtype, int32_t *tile_rows, int32_t *tile_cols,
                               int32_t *tile_tokens);
 
 #ifdef __cplusplus

@@ -238,6 +238,60 @@ forge_status forge_linear_step(const void *X, const void *dY, void *W, void *m, 
     return from_hip(forge_impl::launch_fused(a, md, static_cast<hipStream_t>(stream)));
 }
 
+static_assert(FORGE_MAX_GROUP == forge_impl::MAX_GROUP, "group bound of the ABI and the kernels");
+
+forge_status forge_linear_step_grouped(const forge_matrix *mats, int32_t n, int64_t T, int32_t md,
+                                       float lr, float beta1, float beta2, float eps,
+                                       float weight_decay, int64_t step, void *stream)
+{
+    forge_status s;
+    if ((s = check_dtype_moment(md)) != FORGE_OK) return s;
+    if (!mats) return FORGE_ERR_NULL_POINTER;
+    if (n < 1 || n > FORGE_MAX_GROUP) return FORGE_ERR_INVALID_SHAPE;
+    StateSet st[FORGE_MAX_GROUP];
+    int live[FORGE_MAX_GROUP];
+    int nlive = 0;
+    for (int i = 0; i < n; ++i) {
+        const forge_matrix &x = mats[i];
+        bool empty = false;
+        if ((s = check_shape(T, x.d_in, x.d_out, empty)) != FORGE_OK) return s;
+        if (empty) continue;
+        if ((s = check_inputs(x.X, x.dY, T, x.d_in, x.d_out)) != FORGE_OK) return s;
+        if ((s = check_state(x.W, x.m, x.v, x.m_scale, x.v_scale, x.d_in, x.d_out, md, st[nlive])) != FORGE_OK)
+            return s;
+        live[nlive++] = i;
+    }
+    if (nlive == 0) return FORGE_OK;
+    if ((s = check_hyper(lr, beta1, beta2, eps, weight_decay, step)) != FORGE_OK) return s;
+    for (int a = 0; a < nlive; ++a) {
+        for (int b = 0; b < nlive; ++b) {
+            const forge_matrix &y = mats[live[b]];
+            if (T > 0 && (!disjoint_from(st[a], range_of(y.X, 2 * T * y.d_in)) ||
+                          !disjoint_from(st[a], range_of(y.dY, 2 * T * y.d_out))))
+                return FORGE_ERR_ALIASING;
+            if (b > a)
+                for (int k = 0; k < st[b].n; ++k)
+                    if (!disjoint_from(st[a], st[b].r[k])) return FORGE_ERR_ALIASING;
+        }
+    }
+    if ((s = check_device()) != FORGE_OK) return s;
+
+    const Hyper h = make_hyper(lr, beta1, beta2, eps, weight_decay, step);
+    Args args[FORGE_MAX_GROUP];
+    for (int k = 0; k < nlive; ++k) {
+        const forge_matrix &x = mats[live[k]];
+        Args &a = args[k];
+        a = base_args(x.X, x.dY, T, x.d_in, x.d_out);
+        a.W = static_cast<uint16_t *>(x.W);
+        a.m = x.m;
+        a.v = x.v;
+        a.ms = x.m_scale;
+        a.vs = x.v_scale;
+        a.h = h;
+    }
+    return from_hip(forge_impl::launch_fused_group(args, nlive, md, static_cast<hipStream_t>(stream)));
+}
+
 forge_status forge_wgrad(const void *X, const void *dY, void *G, int64_t T, int64_t d_in,
                          int64_t d_out, int32_t gd, void *stream)
 {

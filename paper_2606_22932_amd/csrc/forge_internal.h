@@ -32,6 +32,17 @@ struct Args {
     Hyper h;
 };
 
+// Up to this many independent matrices share one fused launch (forge_linear_step_grouped).
+constexpr int MAX_GROUP = 8;
+
+// A launch over several matrices: their tiles are concatenated, matrix i owning global
+// tiles [start[i], start[i+1]).  Passed by value as the kernel argument (about 1 KB).
+struct GroupArgs {
+    Args a[MAX_GROUP];
+    int start[MAX_GROUP + 1];
+    int n;
+};
+
 enum MomentKind { MK_F32 = 0, MK_BF16 = 1, MK_I8 = 2 };
 enum EpiKind { EPI_ADAMW = 0, EPI_STORE_BF16 = 1, EPI_STORE_F32 = 2 };
 
@@ -42,6 +53,8 @@ TileShape tile_shape(int moment_kind);
 
 // Launchers; they return the hipError_t of the launch.
 hipError_t launch_fused(const Args &a, int moment_kind, hipStream_t stream);
+// n matrices (1 <= n <= MAX_GROUP, none empty) in one launch; all share T and the step.
+hipError_t launch_fused_group(const Args *a, int n, int moment_kind, hipStream_t stream);
 hipError_t launch_wgrad(const Args &a, int grad_f32, hipStream_t stream);
 hipError_t launch_adamw(const Args &a, int moment_kind, int grad_f32, hipStream_t stream);
 

@@ -90,14 +90,18 @@ __device__ __forceinline__ void adamw_elem(float g, float w, float m, float v, c
 }
 
 // Workgroups are dispatched round-robin over the 8 XCDs (each with its own L2): give
-// each XCD a contiguous run of tiles, and walk that run in groups of `group_p` tile rows
-// so that concurrently resident tiles share their dY row slabs and X column slabs.
-__device__ __forceinline__ void tile_of(int bid, int ntiles, int tiles_p, int tiles_q,
-                                        int group_p, int &tp, int &tq)
+// each XCD a contiguous run of the ntiles tiles of a launch.
+__device__ __forceinline__ int xcd_remap(int bid, int ntiles)
 {
     const int k = ntiles >> 3, r = ntiles & 7;
     const int x = bid & 7, s = bid >> 3;
-    const int t = (x < r) ? x * (k + 1) + s : r * (k + 1) + (x - r) * k + s;
+    return (x < r) ? x * (k + 1) + s : r * (k + 1) + (x - r) * k + s;
+}
+
+// Tile t of one matrix in groups of `group_p` tile rows, so that concurrently resident
+// tiles share their dY row slabs and X column slabs.
+__device__ __forceinline__ void raster(int t, int tiles_p, int tiles_q, int group_p, int &tp, int &tq)
+{
     const int per_group = group_p * tiles_q;
     const int g = t / per_group;
     const int first = g * group_p;
@@ -105,6 +109,12 @@ __device__ __forceinline__ void tile_of(int bid, int ntiles, int tiles_p, int ti
     const int within = t - g * per_group;
     tp = first + within % gsz;
     tq = within / gsz;
+}
+
+__device__ __forceinline__ void tile_of(int bid, int ntiles, int tiles_p, int tiles_q,
+                                        int group_p, int &tp, int &tq)
+{
+    raster(xcd_remap(bid, ntiles), tiles_p, tiles_q, group_p, tp, tq);
 }
 
 // ------------------------------------------------------------------------ mainloop
@@ -653,7 +663,7 @@ __device__ __forceinline__ void epi_store_g(const Args &a, int p0, int q0, int s
 // ------------------------------------------------------------------------ kernels
 
 template <int BP, int BQ, int MK, int EPI>
-__global__ void __launch_bounds__(NT, 2) fused_kernel(Args a)
+__global__ void __launch_bounds__(NT, 2) fused_kernel(GroupArgs g)
 {
     using ML = Mainloop<BP, BQ, (MK == MK_I8 ? 3 : NSTAGE), (MK == MK_I8 ? 32 : TK128)>;
     using EM = EpiMap<BP, BQ>;
@@ -667,10 +677,16 @@ __global__ void __launch_bounds__(NT, 2) fused_kernel(Args a)
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int lane = tid & 63;
     const int s = tid - NROLE;
+    // This workgroup's tile: XCD-aware over all tiles of the group, then the matrix that
+    // owns it and the tile's place in that matrix.
+    const int t = xcd_remap(blockIdx.x, g.start[g.n]);
+    int mi = 0;
+    while (mi + 1 < g.n && t >= g.start[mi + 1]) ++mi;
+    const Args a = g.a[mi];
     const int nbar = ML::nbar(a.T);
     {
         int tp, tq;
-        tile_of(blockIdx.x, a.tiles_p * a.tiles_q, a.tiles_p, a.tiles_q, a.group_p, tp, tq);
+        raster(t - g.start[mi], a.tiles_p, a.tiles_q, a.group_p, tp, tq);
         const int p0 = tp * BP, q0 = tq * BQ;
         if (wave < 4) {
             ML ml;
@@ -767,31 +783,43 @@ static Args with_grid(Args a, int bp, int bq, int &ntiles)
     return a;
 }
 
-hipError_t launch_fused(const Args &a0, int mk, hipStream_t st)
+// Tile grid of each matrix, prefix sums of their tile counts, and the launch.
+template <int BP, int BQ, int MK, int EPI>
+static hipError_t launch_group(const Args *a, int n, hipStream_t st)
 {
-    int n;
-    if (mk == MK_I8) {
-        Args a = with_grid(a0, BP_I8, BQ_I8, n);
-        hipLaunchKernelGGL((fused_kernel<BP_I8, BQ_I8, MK_I8, EPI_ADAMW>), dim3(n), dim3(NT), 0, st, a);
-    } else if (mk == MK_BF16) {
-        Args a = with_grid(a0, BP_F, BQ_F, n);
-        hipLaunchKernelGGL((fused_kernel<BP_F, BQ_F, MK_BF16, EPI_ADAMW>), dim3(n), dim3(NT), 0, st, a);
-    } else {
-        Args a = with_grid(a0, BP_F, BQ_F, n);
-        hipLaunchKernelGGL((fused_kernel<BP_F, BQ_F, MK_F32, EPI_ADAMW>), dim3(n), dim3(NT), 0, st, a);
+    GroupArgs g;
+    g.n = n;
+    g.start[0] = 0;
+    for (int i = 0; i < n; ++i) {
+        int nt;
+        g.a[i] = with_grid(a[i], BP, BQ, nt);
+        g.start[i + 1] = g.start[i] + nt;
     }
+    for (int i = n; i < MAX_GROUP; ++i) {
+        g.a[i] = g.a[0];
+        g.start[i + 1] = g.start[n];
+    }
+    if (g.start[n] == 0) return hipSuccess;
+    hipLaunchKernelGGL((fused_kernel<BP, BQ, MK, EPI>), dim3(g.start[n]), dim3(NT), 0, st, g);
     return hipGetLastError();
 }
 
-hipError_t launch_wgrad(const Args &a0, int grad_f32, hipStream_t st)
+hipError_t launch_fused_group(const Args *a, int n, int mk, hipStream_t st)
 {
-    int n;
-    Args a = with_grid(a0, BP_F, BQ_F, n);
-    if (grad_f32)
-        hipLaunchKernelGGL((fused_kernel<BP_F, BQ_F, MK_BF16, EPI_STORE_F32>), dim3(n), dim3(NT), 0, st, a);
-    else
-        hipLaunchKernelGGL((fused_kernel<BP_F, BQ_F, MK_BF16, EPI_STORE_BF16>), dim3(n), dim3(NT), 0, st, a);
-    return hipGetLastError();
+    if (mk == MK_I8) return launch_group<BP_I8, BQ_I8, MK_I8, EPI_ADAMW>(a, n, st);
+    if (mk == MK_BF16) return launch_group<BP_F, BQ_F, MK_BF16, EPI_ADAMW>(a, n, st);
+    return launch_group<BP_F, BQ_F, MK_F32, EPI_ADAMW>(a, n, st);
+}
+
+hipError_t launch_fused(const Args &a, int mk, hipStream_t st)
+{
+    return launch_fused_group(&a, 1, mk, st);
+}
+
+hipError_t launch_wgrad(const Args &a, int grad_f32, hipStream_t st)
+{
+    if (grad_f32) return launch_group<BP_F, BQ_F, MK_BF16, EPI_STORE_F32>(&a, 1, st);
+    return launch_group<BP_F, BQ_F, MK_BF16, EPI_STORE_BF16>(&a, 1, st);
 }
 
 hipError_t launch_adamw(const Args &a0, int mk, int grad_f32, hipStream_t st)

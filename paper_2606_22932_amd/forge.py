@@ -37,8 +37,19 @@ _lock = threading.Lock()
 _lib = None
 
 _P, _I64, _I32, _F = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_float
+FORGE_MAX_GROUP = 8
+
+
+class forge_matrix(ctypes.Structure):
+    """``forge_matrix`` of ``include/forge.h``: one matrix of a grouped step."""
+    _fields_ = [("X", _P), ("dY", _P), ("W", _P), ("m", _P), ("v", _P), ("m_scale", _P),
+                ("v_scale", _P), ("d_in", _I64), ("d_out", _I64)]
+
+
 _SIGS = {
     "forge_linear_step": [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I32, _F, _F, _F, _F, _F, _I64, _P],
+    "forge_linear_step_grouped": [ctypes.POINTER(forge_matrix), _I32, _I64, _I32, _F, _F, _F, _F, _F,
+                                  _I64, _P],
     "forge_wgrad": [_P, _P, _P, _I64, _I64, _I64, _I32, _P],
     "forge_adamw": [_P, _I32, _P, _P, _P, _P, _P, _I64, _I64, _I32, _F, _F, _F, _F, _F, _I64, _P],
     "forge_linear_step_unfused": [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I32, _F, _F, _F, _F,
@@ -147,6 +158,33 @@ def forge_linear_step(X, dY, W, m, v, m_scale=None, v_scale=None, *, lr, beta1, 
                                  _ptr(v_scale), T, d_in, d_out, _moment_code(m), lr, beta1, beta2,
                                  eps, weight_decay, int(step), _stream(stream, W))
     _check(st, "forge_linear_step")
+
+
+def forge_linear_step_grouped(mats, *, lr, beta1, beta2, eps, weight_decay, step, stream=None):
+    """The fused step on several independent matrices in one launch.
+
+    ``mats``: sequence of ``(X, dY, W, m, v)`` or ``(X, dY, W, m, v, m_scale, v_scale)``
+    tuples sharing the token count T and the moment dtype (at most FORGE_MAX_GROUP).
+    """
+    mats = [tuple(x) + (None,) * (7 - len(x)) for x in mats]
+    if not mats:
+        raise ValueError("empty group")
+    arr = (forge_matrix * len(mats))()
+    T = code = None
+    for i, (X, dY, W, m, v, ms, vs) in enumerate(mats):
+        _dev(X, dY, W, m, v, ms, vs)
+        Ti, d_in, d_out = _shapes(X, dY, W)
+        ci = _moment_code(m)
+        if T is None:
+            T, code = Ti, ci
+        elif Ti != T or ci != code:
+            raise ValueError("all matrices of a group share T and the moment dtype")
+        arr[i] = forge_matrix(X.data_ptr(), dY.data_ptr(), W.data_ptr(), m.data_ptr(), v.data_ptr(),
+                              None if ms is None else ms.data_ptr(), None if vs is None else vs.data_ptr(),
+                              d_in, d_out)
+    st = lib().forge_linear_step_grouped(arr, len(mats), T, code, lr, beta1, beta2, eps, weight_decay,
+                                         int(step), _stream(stream, mats[0][2]))
+    _check(st, "forge_linear_step_grouped")
 
 
 def forge_wgrad(X, dY, G, *, stream=None):

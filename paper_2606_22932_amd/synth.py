@@ -81,6 +81,27 @@ def _sweep_matrices():
     return tuple(mats)
 
 
+def launch_groups(wl: "Workload"):
+    """Indices into ``wl.matrices`` per fused launch, in the order a backward pass makes
+    the weight gradients available.
+
+    For the sweep: lm_head first, then each decoder layer from the last to the first as
+    [down], [gate, up], [o], [q, k, v] -- gate and up (and q, k, v) read the same input and
+    receive their upstream gradients together, so one grouped launch steps them.  Other
+    workloads: one matrix per launch.
+    """
+    if wl.name != "sweep":
+        return [[i] for i in range(len(wl.matrices))]
+    per = len(LLAMA8B_PROJ)
+    idx = {nm: j for j, (nm, _, _) in enumerate(LLAMA8B_PROJ)}
+    groups = [[32 * per]]
+    for layer in reversed(range(32)):
+        b = layer * per
+        groups += [[b + idx["down"]], [b + idx["gate"], b + idx["up"]], [b + idx["o"]],
+                   [b + idx["q"], b + idx["k"], b + idx["v"]]]
+    return groups
+
+
 WORKLOADS = {
     "layer256": Workload("layer256", 128, (Matrix("layer256", 256, 256, 0),), "f32",
                          x_std=1.0, dy_std=0.01, m_std=0.0, v_std=0.0, steps=(1, 2, 3)),

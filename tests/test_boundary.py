@@ -159,3 +159,58 @@ def test_paper_bytes_per_parameter():
     assert accounting.fused_bytes(T, d, d, "bf16") / P == g["fused_bf16"]
     assert accounting.unfused_bytes(T, d, d, "bf16", "bf16") / P == g["standard_bf16"]
     assert g["standard_bf16"] / g["fused_bf16"] == pytest.approx(g["memory_bound_speedup_bound"], abs=0.005)  # printed to 2 decimals
+
+
+# ----------------------------------------------------------------------------- grouped step
+
+def _mat(i, d_in=128, d_out=256, **over):
+    """Fake descriptor of matrix i: its own X, dY, W, m, v, scales, 1 GiB apart."""
+    base = (100 + 16 * i) * GiB
+    f = dict(X=base, dY=base + GiB, W=base + 2 * GiB, m=base + 3 * GiB, v=base + 4 * GiB,
+             ms=base + 5 * GiB, vs=base + 6 * GiB, d_in=d_in, d_out=d_out)
+    f.update(over)
+    return forge.forge_matrix(f["X"], f["dY"], f["W"], f["m"], f["v"], f["ms"], f["vs"], f["d_in"], f["d_out"])
+
+
+def call_group(mats, T=64, md=BF16, n=None, **over):
+    hp = dict(HP)
+    hp.update(over)
+    arr = (forge.forge_matrix * max(1, len(mats)))(*mats)
+    return lib().forge_linear_step_grouped(arr, len(mats) if n is None else n, T, md, hp["lr"], hp["beta1"],
+                                           hp["beta2"], hp["eps"], hp["wd"], hp["step"], None)
+
+
+def test_group_count_and_null_errors():
+    assert lib().forge_linear_step_grouped(None, 1, 64, BF16, 1e-3, 0.9, 0.999, 1e-8, 0.1, 1, None) == NULLP
+    assert call_group([_mat(0)], n=0) == SHAPE
+    assert call_group([_mat(i) for i in range(forge.FORGE_MAX_GROUP + 1)]) == SHAPE
+    assert call_group([_mat(0)], md=9) == DTYPE
+
+
+def test_group_checks_every_matrix():
+    assert call_group([_mat(0), _mat(1, d_in=12)]) == UNSUP
+    assert call_group([_mat(0), _mat(1, W=0)]) == NULLP
+    assert call_group([_mat(0), _mat(1, m=(116 * GiB) + 3 * GiB + 2)]) == MISAL
+    assert call_group([_mat(0), _mat(1, v=(116 * GiB) + 2 * GiB + 16)]) == ALIAS   # v inside W, same matrix
+    assert call_group([_mat(0), _mat(1)], step=0) == HYPER
+
+
+def test_group_aliasing_across_matrices():
+    m0 = _mat(0)
+    # the state of matrix 1 overlapping the state of matrix 0
+    assert call_group([m0, _mat(1, W=m0.m + 64)]) == ALIAS
+    # the state of matrix 1 overlapping the input of matrix 0
+    assert call_group([m0, _mat(1, v=m0.X)]) == ALIAS
+    assert call_group([m0, _mat(1, W=m0.dY + 16)]) == ALIAS
+
+
+def test_group_all_empty_is_a_noop():
+    assert call_group([_mat(0, d_in=0), _mat(1, d_out=0)]) == OK
+
+
+@pytest.mark.skipif(_gpu_visible(), reason="on a GPU machine a valid call would launch on fake pointers")
+def test_group_valid_arguments_reach_the_device_check():
+    # q, k, v style: three matrices sharing X (read-only inputs may be shared)
+    m0 = _mat(0)
+    assert call_group([m0, _mat(1, X=m0.X), _mat(2, X=m0.X)]) == NODEV
+    assert call_group([_mat(0), _mat(1, d_in=0)], T=0) == NODEV

@@ -6,7 +6,8 @@ X).  So the oracle run on a subset of rows (or columns) gives exactly the values
 full problem has there, and a full-size GPU result can be checked on a sample.
 
 * The Llama-3.1-8B sweep (225 matrices, T=512, bf16 moments) is stepped exactly as the
-  benchmark times it: ``forge_linear_step`` per matrix, back to back on one stream.
+  benchmark times it: ``forge_linear_step_grouped`` per backward-order group of matrices
+  (``synth.launch_groups``), back to back on one stream.
 * The largest legal operands: X or dY with just under 2^31 elements and a ragged token
   count, so the last token chunk runs past T at byte offsets beyond 2^32.
 """
@@ -51,9 +52,10 @@ def test_sweep_sampled_rows_in_bench_configuration():
                     bits(m.index_select(0, r)), bits(v.index_select(0, r)), "bf16", hp=dict(wl.hyper))
         expected.append((mat, r, p, run_oracle(p, step)))
         tensors.append((X, dY, W, m, v))
-    _say(f"sweep: {len(tensors)} matrices generated; one fused step")
-    for X, dY, W, m, v in tensors:
-        forge.forge_linear_step(X, dY, W, m, v, step=step, **wl.hyper)
+    groups = synth.launch_groups(wl)
+    _say(f"sweep: {len(tensors)} matrices generated; one fused step in {len(groups)} grouped launches")
+    for g in groups:
+        forge.forge_linear_step_grouped([tensors[i] for i in g], step=step, **wl.hyper)
     torch.cuda.synchronize()
     n = 0
     for (X, dY, W, m, v), (mat, r, p, ora) in zip(tensors, expected):

@@ -198,3 +198,57 @@ def test_stream_argument_is_honoured():
     s.synchronize()
     ora = run_oracle(p, 3)
     check_step(dict(W=bits(W), m=bits(m), v=bits(v)), ora, "bf16", hp=p.hp)
+
+
+def _state_on_gpu(p):
+    st = [dev(a) for a in (p.W, p.m, p.v)]
+    sc = [dev(p.m_scale), dev(p.v_scale)] if p.m_scale is not None else [None, None]
+    return st + sc
+
+
+@pytest.mark.parametrize("moment", ["f32", "bf16", "i8"])
+def test_grouped_matches_oracle_and_single_calls(moment):
+    """forge_linear_step_grouped: every matrix as the oracle has it, and bit-identical to
+    a separate forge_linear_step call on that matrix (Def. 1: tiles are independent)."""
+    T = 77
+    shapes = [(328, 200), (136, 264), (8, 8), (1032, 776), (392, 520)]
+    probs = [make_problem(T, d_in, d_out, moment, seed=40 + i) for i, (d_in, d_out) in enumerate(shapes)]
+    _say(f"grouped {moment}: {len(probs)} matrices, T={T}")
+    group, single = [], []
+    for p in probs:
+        X, dY = dev(p.X), dev(p.dY)
+        W, m, v, ms, vs = _state_on_gpu(p)
+        group.append((X, dY, W, m, v, ms, vs))
+        W2, m2, v2, ms2, vs2 = _state_on_gpu(p)
+        forge.forge_linear_step(X, dY, W2, m2, v2, ms2, vs2, step=100, **p.hp)
+        single.append((W2, m2, v2, ms2, vs2))
+    forge.forge_linear_step_grouped(group, step=100, **probs[0].hp)
+    torch.cuda.synchronize()
+    for p, g, s1 in zip(probs, group, single):
+        out = dict(W=bits(g[2]), m=bits(g[3]), v=bits(g[4]))
+        if moment == "i8":
+            out.update(m_scale=bits(g[5]), v_scale=bits(g[6]))
+        _say(check_step(out, run_oracle(p, 100), moment, hp=p.hp))
+        for a, b in zip(g[2:], s1):
+            if a is not None:
+                assert torch.equal(a.view(torch.uint8), b.view(torch.uint8)), "grouped != single call"
+
+
+def test_grouped_shared_input_and_empty_member():
+    """q, k, v style: three matrices read the same X; an empty matrix in the group is skipped."""
+    T, d_in = 96, 264
+    X = synth.gaussian((T, d_in), 1.0, 5101, device="cuda")
+    members, probs = [], []
+    for i, d_out in enumerate((392, 136, 136)):
+        dY = synth.gaussian((T, d_out), 1e-3, 5111 + i, device="cuda")
+        W = synth.gaussian((d_out, d_in), 0.02, 5121 + i, device="cuda")
+        m = synth.gaussian((d_out, d_in), 1e-4, 5131 + i, device="cuda")
+        v = synth.gaussian((d_out, d_in), 1e-6, 5141 + i, device="cuda", absolute=True)
+        probs.append(Problem(bits(X), bits(dY), bits(W), bits(m), bits(v), "bf16"))
+        members.append((X, dY, W, m, v))
+    e = torch.empty((0, d_in), dtype=torch.bfloat16, device="cuda")
+    members.insert(1, (X, torch.empty((T, 0), dtype=torch.bfloat16, device="cuda"), e, e.clone(), e.clone()))
+    forge.forge_linear_step_grouped(members, step=7, **probs[0].hp)
+    torch.cuda.synchronize()
+    for p, (_, _, W, m, v) in zip(probs, [members[0], members[2], members[3]]):
+        _say(check_step(dict(W=bits(W), m=bits(m), v=bits(v)), run_oracle(p, 7), "bf16", hp=p.hp))
