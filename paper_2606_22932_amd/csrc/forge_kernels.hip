@@ -34,6 +34,9 @@ typedef short v4i16_t __attribute__((ext_vector_type(4)));
 #ifndef FORGE_NS
 #define FORGE_NS 4
 #endif
+#ifndef FORGE_GROUP_P             // tile rows walked together by the raster (0: by shape)
+#define FORGE_GROUP_P 0
+#endif
 constexpr int TK128 = FORGE_TK;   // tokens per pipeline chunk (the GEMM's K step), 128x128 tiles
 constexpr int NSTAGE = FORGE_NS;  // LDS ring depth (chunks) of the 128x128 mainloop
 constexpr int NROLE = 256;      // threads per role (4 waves)
@@ -774,11 +777,22 @@ TileShape tile_shape(int mk)
     return TileShape{BP_F, BQ_F, TK128};
 }
 
+// Tile rows per raster group, by the shape of the tile grid (measured on the Llama-3.1-8B
+// shapes at T = 512): matrices wider than tall walk 24 rows at a time, very tall ones 8,
+// the rest 16.  The 64 tiles resident on an XCD then span a few hundred KB of operand
+// slabs in its L2 and a few thousand rows of the state, in runs of 0.7-2 KB per row.
+static int raster_rows(int tiles_p, int tiles_q)
+{
+    if (tiles_q > tiles_p) return 24;
+    if (tiles_p > 16 * tiles_q) return 8;
+    return 16;
+}
+
 static Args with_grid(Args a, int bp, int bq, int &ntiles)
 {
     a.tiles_p = (a.d_out + bp - 1) / bp;
     a.tiles_q = (a.d_in + bq - 1) / bq;
-    a.group_p = 8;
+    a.group_p = FORGE_GROUP_P ? FORGE_GROUP_P : raster_rows(a.tiles_p, a.tiles_q);
     ntiles = a.tiles_p * a.tiles_q;
     return a;
 }
