@@ -11,6 +11,7 @@ Prints one JSON line on stdout; progress goes to stderr.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import json
 import os
 import sys
@@ -31,12 +32,12 @@ COPY_BYTES = 1 << 30           # size of the calibration copy (--copy-calibratio
 # source whose sha256 is recorded: after any change to it the figure is reported as null.
 TRAFFIC = {
     "sweep": {
-        "source_sha256": "f8c737b6e94fd91dd52cf85a2ace6472167e4f4c2d6f767584d3daceea28042c",
-        "fetch_kib_per_launch": 120316.1,     # FETCH_SIZE, mean over the 225 launches
-        "write_kib_per_launch": 195454.6,     # WRITE_SIZE
-        "fetch_scale": 1.99995,               # 1 GiB copy: FETCH_SIZE reads 524302 KiB
+        "source_sha256": "e8a0c54101a87726a11632ad0929ce72932d665a5f87f5818928956c11b250df",
+        "fetch_kib_per_launch": 207370.6,     # FETCH_SIZE, mean over the 129 launches of a step
+        "write_kib_per_launch": 340911.7,     # WRITE_SIZE
+        "fetch_scale": 1.99994,               # 1 GiB copy: FETCH_SIZE reads 524303 KiB
         "write_scale": 1.0,                   # 1 GiB copy: WRITE_SIZE reads 1048576 KiB
-        "bytes_per_launch": 446546218,        # (fetch * fetch_scale + write * write_scale) KiB
+        "bytes_per_launch": 773776101,        # (fetch * fetch_scale + write * write_scale) KiB
     },
 }
 
@@ -166,6 +167,10 @@ def main():
     ap.add_argument("--workload", default="sweep", choices=["sweep", "o_proj", "mlp", "mlp_i8"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
+    ap.add_argument("--tokens", type=int, default=None,
+                    help="override the workload's token count T (0: the state streaming alone)")
+    ap.add_argument("--no-ceilings", action="store_true",
+                    help="skip the measured HBM ceilings (a child process after the timed work)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run a plain 1 GiB device copy first (reference for counter scaling)")
     args = ap.parse_args()
@@ -183,6 +188,11 @@ def main():
     device = torch.device("cuda:0")
     torch.cuda.set_device(device)
     wl = synth.WORKLOADS[args.workload]
+    if args.tokens is not None:
+        if not 0 <= args.tokens <= wl.T:
+            print(f"--tokens must be in [0, {wl.T}]", file=sys.stderr)
+            sys.exit(2)
+        wl = dataclasses.replace(wl, T=args.tokens)
     if args.copy_calibration:
         log(f"calibration copy: {COPY_BYTES} bytes x 3")
         copy_calibration(device)
@@ -230,7 +240,8 @@ def main():
             "workload": {"sweep": "Llama-3.1-8B linear-layer sweep: 32 x {q,k,v,o,gate,up,down} + lm_head, T=512, bf16 W/m/v",
                          "o_proj": "Llama-3.1-8B o_proj 4096x4096, T=512, bf16 W/m/v",
                          "mlp": "Llama-3.1-8B gate/up/down, T=512, bf16 W/m/v",
-                         "mlp_i8": "Llama-3.1-8B gate/up/down, T=512, int8 m/v"}[args.workload],
+                         "mlp_i8": "Llama-3.1-8B gate/up/down, T=512, int8 m/v"}[args.workload]
+                        .replace("T=512", f"T={T}"),
             "T": T, "matrices": len(mats),
             "params": sum(d["mat"].d_in * d["mat"].d_out for d in mats),
             "moments": wl.moment, "algorithmic_bytes_per_step": fused_b,
@@ -271,13 +282,39 @@ def main():
         del G_ws
 
     if not args.no_cpu_baseline:
-        del mats
+        mats = launches = None
         torch.cuda.empty_cache()
         log("timing the CPU oracle on its sample")
         out["cpu_baseline"] = cpu_baseline(synth.WORKLOADS["sweep"], device)
         log(f"cpu baseline: {out['cpu_baseline']}")
 
+    if not args.no_ceilings:
+        mats = launches = None
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        log("measuring HBM ceilings (read / write / copy / in-place read-modify-write of 3 streams)")
+        c = hbm_ceilings()
+        if c is not None:
+            c["fused_over_rmw3"] = round(kern_gbs / c["rmw3"], 4)
+            out["hbm_ceiling"] = c
+            log(f"ceilings: {c}")
+
     print(json.dumps(out), flush=True)
+
+
+def hbm_ceilings():
+    """Measured HBM bandwidth of this device for plain access mixes (context for the
+    roofline): runs the built probe ``paper_2606_22932_amd/hbm_ceiling`` as a child process."""
+    import subprocess
+    from paper_2606_22932_amd import build
+    if not os.path.exists(build.CEILING_BIN):
+        log("hbm_ceiling is not built; skipping the measured ceilings")
+        return None
+    res = subprocess.run([build.CEILING_BIN], capture_output=True, text=True, timeout=300)
+    if res.returncode != 0:
+        log(f"hbm_ceiling failed ({res.returncode}): {res.stderr.strip()}")
+        return None
+    return json.loads(res.stdout.strip().splitlines()[-1])
 
 
 if __name__ == "__main__":

@@ -13,6 +13,9 @@ LIB = os.path.join(HERE, "libforge.so")
 SOURCES = [os.path.join(CSRC, "forge_kernels.hip"), os.path.join(CSRC, "forge_api.cpp")]
 HEADERS = [os.path.join(CSRC, "forge_internal.h"), os.path.join(INCLUDE, "forge.h")]
 
+CEILING_SRC = os.path.join(CSRC, "hbm_ceiling.hip")
+CEILING_BIN = os.path.join(HERE, "hbm_ceiling")   # measured HBM ceilings (bench context)
+
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
@@ -34,7 +37,23 @@ def build(verbose: bool = False) -> str:
     if verbose:
         sys.stderr.write(res.stderr)
     os.replace(tmp, LIB)
+    build_ceiling(verbose)
     return LIB
+
+
+def build_ceiling(verbose: bool = False) -> str:
+    """Compile the stand-alone HBM ceiling probe ``paper_2606_22932_amd/hbm_ceiling``."""
+    tmp = CEILING_BIN + ".tmp"
+    cmd = [HIPCC, "--offload-arch=gfx950", "-O3", "-std=c++17", "-Xclang", "-target-feature", "-Xclang",
+           "-packed-fp32-ops", "-Wall", CEILING_SRC, "-o", tmp]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        sys.stderr.write(res.stdout + res.stderr)
+        raise RuntimeError("hipcc failed building hbm_ceiling")
+    if verbose:
+        sys.stderr.write(res.stderr)
+    os.replace(tmp, CEILING_BIN)
+    return CEILING_BIN
 
 
 def is_stale() -> bool:
