@@ -18,6 +18,8 @@
 // of a materialised G into LDS and runs the same epilogue code.
 #include "forge_internal.h"
 
+#include <mutex>
+
 namespace forge_impl {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
@@ -34,6 +36,13 @@ typedef short v4i16_t __attribute__((ext_vector_type(4)));
 #ifndef FORGE_NS
 #define FORGE_NS 4
 #endif
+#ifndef FORGE_NS_I8P               // ring depth of the pipelined int8 kernel
+#define FORGE_NS_I8P 4
+#endif
+#ifndef FORGE_NSW_I8P              // its stream waves (4 or 8)
+#define FORGE_NSW_I8P 8
+#endif
+constexpr int NS_I8P = FORGE_NS_I8P;
 #ifndef FORGE_GROUP_P             // tile rows walked together by the raster (0: by shape)
 #define FORGE_GROUP_P 0
 #endif
@@ -290,9 +299,10 @@ struct Mainloop {
         }
     }
 
-    // The whole token loop; executes exactly nbar(T) workgroup barriers.
-    __device__ __forceinline__ void run(const Args &a, int p0, int q0, unsigned char *lds, int wave,
-                                        int lane)
+    // Start a tile: zero the accumulators, set up this lane's DMA pieces and fragment
+    // offsets, and issue the first NS-1 chunks into the ring.  No barrier.
+    __device__ __forceinline__ void begin(const Args &a, int p0, int q0, unsigned char *lds, int wave,
+                                          int lane)
     {
 #pragma unroll
         for (int iq = 0; iq < 2; ++iq)
@@ -302,10 +312,17 @@ struct Mainloop {
                 for (int r = 0; r < 16; ++r) acc[iq][ip][r] = 0.0f;
         const int nch = (a.T + TK - 1) / TK;
         setup(a, p0, q0, wave, lane);
-        const uint32_t lds_base = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)lds;
 #pragma unroll
         for (int c = 0; c < NS - 1; ++c)
             if (c < nch) issue(a, lds + c * STAGE_BYTES, c, wave);
+    }
+
+    // The token loop of a tile started with begin(); executes exactly nch(T) workgroup
+    // barriers (one per chunk).
+    __device__ __forceinline__ void body(const Args &a, unsigned char *lds, int wave)
+    {
+        const int nch = (a.T + TK - 1) / TK;
+        const uint32_t lds_base = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)lds;
         for (int c = 0; c < nch; ++c) {
             const int younger = min(NS - 2, nch - 1 - c);
             wait_chunk(younger);
@@ -314,9 +331,18 @@ struct Mainloop {
                 compute(lds_base + (uint32_t)((c % NS) * STAGE_BYTES + h * 32 * XROWB));
             if (c + NS - 1 < nch) issue(a, lds + ((c + NS - 1) % NS) * STAGE_BYTES, c + NS - 1, wave);
         }
+    }
+
+    // The whole token loop; executes exactly nbar(T) workgroup barriers.
+    __device__ __forceinline__ void run(const Args &a, int p0, int q0, unsigned char *lds, int wave,
+                                        int lane)
+    {
+        begin(a, p0, q0, lds, wave, lane);
+        body(a, lds, wave);
         lds_barrier();   // every wave is done reading the stages, which G reuses
     }
 
+    static __device__ __forceinline__ int nch(int T) { return (T + TK - 1) / TK; }
     static __device__ __forceinline__ int nbar(int T) { return (T + TK - 1) / TK + 1; }
 
     // Accumulators -> LDS as G[p][q] (fp32, row pitch GP floats).
@@ -345,11 +371,11 @@ struct Mainloop {
 // Lane mapping shared by every epilogue: 256 lanes, each owning 8 consecutive columns of
 // one row per pass; consecutive lanes walk a row, so every access is a coalesced 16-byte
 // (or 8-byte, int8 codes) vector.
-template <int BP, int BQ>
+template <int BP, int BQ, int NTH = NROLE>
 struct EpiMap {
     static constexpr int GP = BQ + 4;           // LDS G row pitch in floats
     static constexpr int LPR = BQ / 8;          // lanes per row
-    static constexpr int RPP = NROLE / LPR;     // rows per pass
+    static constexpr int RPP = NTH / LPR;       // rows per pass
     static constexpr int NPASS = BP / RPP;
     static constexpr int GS_BYTES = BP * GP * 4;
 };
@@ -769,6 +795,364 @@ __global__ void __launch_bounds__(NROLE, 2) adamw_kernel(Args a)
     }
 }
 
+// ------------------------------------------------ int8 moments: tiles pipelined per CU
+//
+// One workgroup per CU steps a sequence of 256x64 tiles.  Its four math waves run the
+// mainloop of tile k while its four stream waves finish tile k-1 (App. B update of W,
+// block absmax, re-quantisation of m and sqrt(v)) and load tile k's state for the next
+// period.  G reaches the stream waves through an LDS stage of its own, written by the
+// math waves between the barriers H1 and H2 that close each period and read by the
+// stream waves during the next period, before its H1.  Every workgroup barrier is
+// executed by all eight waves: a period has nb = max(nch, 2) barriers (the mainloop's
+// chunk barriers, padded), then H1 and H2.
+
+// Byte offset of element (p, q) of a [rows, ld] tensor with `eb`-byte elements, or an
+// offset past every buffer end (reads zero) when the element lies outside the tensor.
+__device__ __forceinline__ uint32_t elem_off(int p, int q, int rows, int ld, int eb)
+{
+    if (p >= rows || q >= ld) return OOR_OFFSET;
+    const uint64_t off = ((uint64_t)p * (uint64_t)ld + (uint64_t)q) * (uint64_t)eb;
+    return off < OOR_OFFSET ? (uint32_t)off : OOR_OFFSET;
+}
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_of(const void *base, uint64_t bytes)
+{
+    const uint32_t n = bytes < OOR_OFFSET ? (uint32_t)bytes : OOR_OFFSET;
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)n, 0x00020000);
+}
+
+template <int NSW>
+struct StreamI8 {
+    using M = EpiMap<BP_I8, BQ_I8, NSW * 64>;           // 8 lanes per row, 8*NSW rows per pass
+    static constexpr int NPASS = M::NPASS;
+    u32x4_t w[NPASS];                                   // W row of each pass (8 bf16)
+    u32x2_t cm[NPASS], cv[NPASS];                       // m and sqrt(v) codes (8 int8 each)
+    float sm[8], sv[8];                                 // the block's old scales of this lane's columns
+    float am[8], av[8];                                 // absmax partials
+    float rcm[8], rcv[8];                               // reciprocals of the new scales
+
+    // Loads of the state of tile (p0, q0) of matrix a: row I of every pass, then the scales.
+    template <int I>
+    __device__ __forceinline__ void load_w(const Args &a, int p0, int q0, int s)
+    {
+        const int p = p0 + I * M::RPP + s / M::LPR, q = q0 + (s % M::LPR) * 8;
+        const __amdgpu_buffer_rsrc_t r = rsrc_of(a.W, 2ull * (uint64_t)a.d_out * (uint64_t)a.d_in);
+        w[I] = __builtin_amdgcn_raw_buffer_load_b128(r, elem_off(p, q, a.d_out, a.d_in, 2), 0, 2);
+    }
+    template <int I>
+    __device__ __forceinline__ void load_codes(const Args &a, int p0, int q0, int s)
+    {
+        const int p = p0 + I * M::RPP + s / M::LPR, q = q0 + (s % M::LPR) * 8;
+        const uint64_t n = (uint64_t)a.d_out * (uint64_t)a.d_in;
+        const uint32_t off = elem_off(p, q, a.d_out, a.d_in, 1);
+        cm[I] = __builtin_amdgcn_raw_buffer_load_b64(rsrc_of(a.m, n), off, 0, 2);
+        cv[I] = __builtin_amdgcn_raw_buffer_load_b64(rsrc_of(a.v, n), off, 0, 2);
+    }
+    __device__ __forceinline__ void load_scales(const Args &a, int p0, int q0, int s)
+    {
+        const int q = q0 + (s % M::LPR) * 8, blk = p0 / I8_BLOCK, nblk = (a.d_out + I8_BLOCK - 1) / I8_BLOCK;
+        const uint64_t n = 4ull * (uint64_t)nblk * (uint64_t)a.d_in;
+        const uint32_t off = elem_off(blk, q, nblk, a.d_in, 4);
+        const __amdgpu_buffer_rsrc_t rm = rsrc_of(a.ms, n), rv = rsrc_of(a.vs, n);
+        const f32x4_t s0 = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rm, off, 0, 2));
+        const f32x4_t s1 = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rm, off + 16u, 0, 2));
+        const f32x4_t t0 = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rv, off, 0, 2));
+        const f32x4_t t1 = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rv, off + 16u, 0, 2));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            sm[e] = s0[e]; sm[e + 4] = s1[e];
+            sv[e] = t0[e]; sv[e + 4] = t1[e];
+        }
+    }
+    template <int I = 0>
+    __device__ __forceinline__ void load_all(const Args &a, int p0, int q0, int s)
+    {
+        load_w<I>(a, p0, q0, s);
+        load_codes<I>(a, p0, q0, s);
+        if constexpr (I + 1 < NPASS) load_all<I + 1>(a, p0, q0, s);
+        else load_scales(a, p0, q0, s);
+    }
+
+    // Wait once for the slot's loads (issued a period earlier, so long done), then hide
+    // the registers from the compiler's wait tracking: what follows does not wait for the
+    // stores of the previous tile.
+    __device__ __forceinline__ void settle()
+    {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+#pragma unroll
+        for (int i = 0; i < NPASS; ++i) asm volatile("" : "+v"(w[i]), "+v"(cm[i]), "+v"(cv[i]));
+#pragma unroll
+        for (int e = 0; e < 8; ++e) asm volatile("" : "+v"(sm[e]), "+v"(sv[e]));
+    }
+
+    __device__ __forceinline__ void reset()
+    {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) am[e] = av[e] = 0.0f;
+    }
+
+    // G of row I of this lane (8 columns) from the LDS stage.
+    template <int I>
+    static __device__ __forceinline__ void g_row(const float *Gs, int s, float g[8])
+    {
+        const float *gr = Gs + (I * M::RPP + s / M::LPR) * M::GP + (s % M::LPR) * 8;
+        const f32x4_t g0 = *reinterpret_cast<const f32x4_t *>(gr);
+        const f32x4_t g1 = *reinterpret_cast<const f32x4_t *>(gr + 4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            g[e] = g0[e];
+            g[e + 4] = g1[e];
+        }
+    }
+
+    // The element's state before and after the step (App. B: m = s_m q_m, v = (s_v q_v)^2).
+    __device__ __forceinline__ void state_at(const Hyper &h, int i, float g, int e, float &w1, float &m1,
+                                             float &v1, float &rv1) const
+    {
+        const float m0 = sm[e] * EpiAdamWI8<BP_I8, BQ_I8>::code_at(cm[i], e);
+        const float r0 = sv[e] * EpiAdamWI8<BP_I8, BQ_I8>::code_at(cv[i], e);
+        const float w0 = (e & 1) ? bf_hi(w[i][e >> 1]) : bf_lo(w[i][e >> 1]);
+        adamw_elem(g, w0, m0, r0 * r0, h, w1, m1, v1, rv1);
+    }
+
+    // Pass 1, row I of tile (p0, q0): new W (from the unquantised fp32 state), absmax;
+    // then W's registers take row I of the next tile (pn, qn) of matrix an.
+    template <int I>
+    __device__ __forceinline__ void pass1(const Args &a, int p0, int q0, int s, const float *Gs,
+                                          const Args &an, int pn, int qn, bool refill)
+    {
+        const int p = p0 + I * M::RPP + s / M::LPR, q = q0 + (s % M::LPR) * 8;
+        float g[8], wo[8];
+        g_row<I>(Gs, s, g);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            float m1, v1, rv1;
+            state_at(a.h, I, g[e], e, wo[e], m1, v1, rv1);
+            am[e] = fmaxf(am[e], fabsf(m1));
+            av[e] = fmaxf(av[e], rv1);
+        }
+        if (p < a.d_out && q < a.d_in) {
+            u32x4_t wn;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) wn[k] = pack_bf16(wo[2 * k], wo[2 * k + 1]);
+            st_nt<u32x4_t>(a.W + (size_t)p * a.d_in + q, wn);
+        }
+        asm volatile("" ::"v"(w[I]));
+        if (refill) load_w<I>(an, pn, qn, s);
+    }
+
+    // Block absmax of this lane's columns over its rows: within the wave, then (through
+    // LDS, across the barrier that follows) across the NSW stream waves.
+    __device__ __forceinline__ void partials(int s, float *red)
+    {
+        const int qo = (s % M::LPR) * 8;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+#pragma unroll
+            for (int d = M::LPR; d < 64; d <<= 1) {
+                am[e] = fmaxf(am[e], __shfl_xor(am[e], d));
+                av[e] = fmaxf(av[e], __shfl_xor(av[e], d));
+            }
+        }
+        const int sw = s >> 6;
+        if ((s & 63) < M::LPR) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                red[sw * BQ_I8 + qo + e] = am[e];
+                red[NSW * BQ_I8 + sw * BQ_I8 + qo + e] = av[e];
+            }
+        }
+    }
+
+    // After the barrier: the block's new scales s = absmax / 127 (stored), kept as reciprocals.
+    __device__ __forceinline__ void scales(const Args &a, int p0, int q0, int s, const float *red)
+    {
+        const int rs = s / M::LPR, qo = (s % M::LPR) * 8, q = q0 + qo;
+        float scm[8], scv[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            float xm = red[qo + e], xv = red[NSW * BQ_I8 + qo + e];
+#pragma unroll
+            for (int wv = 1; wv < NSW; ++wv) {
+                xm = fmaxf(xm, red[wv * BQ_I8 + qo + e]);
+                xv = fmaxf(xv, red[NSW * BQ_I8 + wv * BQ_I8 + qo + e]);
+            }
+            scm[e] = xm / 127.0f;
+            scv[e] = xv / 127.0f;
+            rcm[e] = scm[e] > 0.0f ? __builtin_amdgcn_rcpf(scm[e]) : 0.0f;
+            rcv[e] = scv[e] > 0.0f ? __builtin_amdgcn_rcpf(scv[e]) : 0.0f;
+        }
+        if (rs == 0 && q < a.d_in) {
+            const size_t so = (size_t)(p0 / I8_BLOCK) * a.d_in + q;
+            st_nt<f32x4_t>(a.ms + so, f32x4_t{scm[0], scm[1], scm[2], scm[3]});
+            st_nt<f32x4_t>(a.ms + so + 4, f32x4_t{scm[4], scm[5], scm[6], scm[7]});
+            st_nt<f32x4_t>(a.vs + so, f32x4_t{scv[0], scv[1], scv[2], scv[3]});
+            st_nt<f32x4_t>(a.vs + so + 4, f32x4_t{scv[4], scv[5], scv[6], scv[7]});
+        }
+    }
+
+    // Pass 2, row I: recompute m' and sqrt(v') (the same instructions as pass 1), re-quantise
+    // them against the new scales (v codes at least 1 in a non-zero block), store the codes;
+    // then the code registers take row I of the next tile.
+    template <int I>
+    __device__ __forceinline__ void pass2(const Args &a, int p0, int q0, int s, const float *Gs,
+                                          const Args &an, int pn, int qn, bool refill)
+    {
+        const int p = p0 + I * M::RPP + s / M::LPR, q = q0 + (s % M::LPR) * 8;
+        uint32_t qm2[2] = {0u, 0u}, qv2[2] = {0u, 0u};
+        float g[8];
+        g_row<I>(Gs, s, g);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            float w1, m1, v1, rv1;
+            state_at(a.h, I, g[e], e, w1, m1, v1, rv1);
+            const float qm = fminf(fmaxf(__builtin_rintf(m1 * rcm[e]), -127.0f), 127.0f);
+            float qv = fminf(fmaxf(__builtin_rintf(rv1 * rcv[e]), 1.0f), 127.0f);
+            if (!(rcv[e] > 0.0f)) qv = 0.0f;
+            qm2[e >> 2] |= ((uint32_t)(int32_t)qm & 0xFFu) << (8 * (e & 3));
+            qv2[e >> 2] |= ((uint32_t)(int32_t)qv & 0xFFu) << (8 * (e & 3));
+        }
+        if (p < a.d_out && q < a.d_in) {
+            const size_t off = (size_t)p * a.d_in + q;
+            st_nt<u32x2_t>(static_cast<int8_t *>(a.m) + off, u32x2_t{qm2[0], qm2[1]});
+            st_nt<u32x2_t>(static_cast<int8_t *>(a.v) + off, u32x2_t{qv2[0], qv2[1]});
+        }
+        asm volatile("" ::"v"(cm[I]), "v"(cv[I]));
+        if (refill) load_codes<I>(an, pn, qn, s);
+    }
+
+    // The whole epilogue of one tile, spread over nb barriers: pass-1 rows over the first
+    // half (the last of those barriers separates the absmax partials from their reads),
+    // pass-2 rows over the second half.  Executes exactly nb barriers.
+    template <int I = 0>
+    __device__ __forceinline__ void p1_all(const Args &a, int p0, int q0, int s, const float *Gs,
+                                           const Args &an, int pn, int qn, bool refill, int half, int &done,
+                                           float *red)
+    {
+        pass1<I>(a, p0, q0, s, Gs, an, pn, qn, refill);
+        if constexpr (I + 1 < NPASS) {
+            for (const int t = ((I + 1) * half) / NPASS; done < t && done < half - 1; ++done) lds_barrier();
+            p1_all<I + 1>(a, p0, q0, s, Gs, an, pn, qn, refill, half, done, red);
+        } else {
+            for (; done < half - 1; ++done) lds_barrier();
+            partials(s, red);
+            lds_barrier();
+            ++done;
+        }
+    }
+    template <int I = 0>
+    __device__ __forceinline__ void p2_all(const Args &a, int p0, int q0, int s, const float *Gs,
+                                           const Args &an, int pn, int qn, bool refill, int half, int nb,
+                                           int &done)
+    {
+        pass2<I>(a, p0, q0, s, Gs, an, pn, qn, refill);
+        const int t = half + ((I + 1) * (nb - half)) / NPASS;
+        for (; done < t; ++done) lds_barrier();
+        if constexpr (I + 1 < NPASS) p2_all<I + 1>(a, p0, q0, s, Gs, an, pn, qn, refill, half, nb, done);
+    }
+    // G of the tile stays in its LDS stage until this returns (the math waves overwrite
+    // it only after the next H1).
+    __device__ __forceinline__ void tile(const Args &a, int p0, int q0, int s, const float *Gs,
+                                         const Args &an, int pn, int qn, bool refill, int nb, float *red)
+    {
+        const int half = nb / 2;
+        int done = 0;
+        reset();
+        p1_all(a, p0, q0, s, Gs, an, pn, qn, refill, half, done, red);
+        scales(a, p0, q0, s, red);
+        // Hide the codes and scales from common-subexpression elimination, so that pass 2
+        // recomputes m' and sqrt(v') (bit-identical: the same instructions) instead of
+        // keeping 128 dequantised values from pass 1 alive.
+#pragma unroll
+        for (int i = 0; i < NPASS; ++i) asm volatile("" : "+v"(cm[i]), "+v"(cv[i]));
+#pragma unroll
+        for (int e = 0; e < 8; ++e) asm volatile("" : "+v"(sm[e]), "+v"(sv[e]));
+        p2_all(a, p0, q0, s, Gs, an, pn, qn, refill, half, nb, done);
+        if (refill) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) asm volatile("" ::"v"(sm[e]), "v"(sv[e]));
+            load_scales(an, pn, qn, s);
+        }
+    }
+};
+
+constexpr int NSW_I8P = FORGE_NSW_I8P;                  // stream waves of the pipelined int8 kernel
+constexpr int NT_I8P = NROLE + NSW_I8P * 64;
+
+__global__ void __launch_bounds__(NT_I8P, NT_I8P / 256) pipelined_i8_kernel(GroupArgs g)
+{
+    using ML = Mainloop<BP_I8, BQ_I8, NS_I8P, 32>;
+    using EM = EpiMap<BP_I8, BQ_I8, NSW_I8P * 64>;
+    constexpr int RED_BYTES = 2 * NSW_I8P * BQ_I8 * 4;
+    __shared__ __attribute__((aligned(16))) unsigned char smem[EM::GS_BYTES + ML::LDS_BYTES + RED_BYTES];
+    float *Gs = reinterpret_cast<float *>(smem);
+    unsigned char *ring = smem + EM::GS_BYTES;
+    float *red = reinterpret_cast<float *>(smem + EM::GS_BYTES + ML::LDS_BYTES);
+
+    const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int lane = tid & 63;
+    const int total = g.start[g.n];
+    const int K = (total - (int)blockIdx.x + (int)gridDim.x - 1) / (int)gridDim.x;   // tiles of this workgroup
+    // tile k of this workgroup: its matrix and origin
+    auto locate = [&](int k, int &mi, int &p0, int &q0) {
+        const int t = xcd_remap((int)blockIdx.x + k * (int)gridDim.x, total);
+        mi = 0;
+        while (mi + 1 < g.n && t >= g.start[mi + 1]) ++mi;
+        int tp, tq;
+        raster(t - g.start[mi], g.a[mi].tiles_p, g.a[mi].tiles_q, g.a[mi].group_p, tp, tq);
+        p0 = tp * BP_I8;
+        q0 = tq * BQ_I8;
+    };
+    const int nch = ML::nch(g.a[0].T);
+    const int nb = nch > 2 ? nch : 2;
+
+    if (wave < 4) {
+        ML ml;
+        int mi, p0, q0;
+        locate(0, mi, p0, q0);
+        ml.begin(g.a[mi], p0, q0, ring, wave, lane);
+        for (int k = 0; k < K; ++k) {
+            ml.body(g.a[mi], ring, wave);
+            for (int c = nch; c < nb; ++c) lds_barrier();
+            lds_barrier();                                   // H1: the stream waves hold G(k-1)
+            ml.template stage_g<EM::GP>(Gs, wave, lane);
+            if (k + 1 < K) {
+                locate(k + 1, mi, p0, q0);
+                ml.begin(g.a[mi], p0, q0, ring, wave, lane);
+            }
+            lds_barrier();                                   // H2: G(k) is in LDS
+        }
+        // the stream waves finish the last tile with nb more barriers
+        for (int c = 0; c < nb; ++c) lds_barrier();
+        return;
+    }
+
+    const int s = tid - NROLE;
+    StreamI8<NSW_I8P> st;
+    int mp, pp, qp;                                          // the tile whose state is in the slot
+    locate(0, mp, pp, qp);
+    st.load_all(g.a[mp], pp, qp, s);
+    for (int c = 0; c < nb; ++c) lds_barrier();              // period 0: nothing to finish yet
+    lds_barrier();                                           // H1
+    lds_barrier();                                           // H2
+    for (int k = 1; k <= K; ++k) {
+        // finish tile k-1; during it, load tile k's state (for the next period)
+        st.settle();
+        int mk = mp, pk = pp, qk = qp;
+        const bool more = k < K;
+        if (more) locate(k, mk, pk, qk);
+        st.tile(g.a[mp], pp, qp, s, Gs, g.a[mk], pk, qk, more, nb, red);
+        if (more) {
+            lds_barrier();                                   // H1
+            lds_barrier();                                   // H2
+        }
+        mp = mk;
+        pp = pk;
+        qp = qk;
+    }
+}
+
 // ------------------------------------------------------------------------ launchers
 
 TileShape tile_shape(int mk)
@@ -818,9 +1202,48 @@ static hipError_t launch_group(const Args *a, int n, hipStream_t st)
     return hipGetLastError();
 }
 
+// Compute units of the current device (cached per device ordinal).
+static int cu_count()
+{
+    static std::mutex mu;
+    static int known[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    std::lock_guard<std::mutex> lock(mu);
+    if (known[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+        known[dev] = n;
+    }
+    return known[dev];
+}
+
+// int8 moments: one persistent workgroup per CU, tiles pipelined (pipelined_i8_kernel).
+static hipError_t launch_i8_pipelined(const Args *a, int n, hipStream_t st)
+{
+    GroupArgs g;
+    g.n = n;
+    g.start[0] = 0;
+    for (int i = 0; i < n; ++i) {
+        int nt;
+        g.a[i] = with_grid(a[i], BP_I8, BQ_I8, nt);
+        g.start[i + 1] = g.start[i] + nt;
+    }
+    for (int i = n; i < MAX_GROUP; ++i) {
+        g.a[i] = g.a[0];
+        g.start[i + 1] = g.start[n];
+    }
+    const int total = g.start[n];
+    if (total == 0) return hipSuccess;
+    const int ncu = cu_count();
+    const int grid = total < ncu ? total : ncu;
+    hipLaunchKernelGGL(pipelined_i8_kernel, dim3(grid), dim3(NT_I8P), 0, st, g);
+    return hipGetLastError();
+}
+
 hipError_t launch_fused_group(const Args *a, int n, int mk, hipStream_t st)
 {
-    if (mk == MK_I8) return launch_group<BP_I8, BQ_I8, MK_I8, EPI_ADAMW>(a, n, st);
+    if (mk == MK_I8) return launch_i8_pipelined(a, n, st);
     if (mk == MK_BF16) return launch_group<BP_F, BQ_F, MK_BF16, EPI_ADAMW>(a, n, st);
     return launch_group<BP_F, BQ_F, MK_F32, EPI_ADAMW>(a, n, st);
 }

@@ -252,3 +252,15 @@ def test_grouped_shared_input_and_empty_member():
     torch.cuda.synchronize()
     for p, (_, _, W, m, v) in zip(probs, [members[0], members[2], members[3]]):
         _say(check_step(dict(W=bits(W), m=bits(m), v=bits(v)), run_oracle(p, 7), "bf16", hp=p.hp))
+
+
+@pytest.mark.parametrize("shape", [(512, 520, 776), (77, 328, 264), (0, 64, 256)], ids=lambda s: "x".join(map(str, s)))
+def test_int8_fused_equals_unfused_fp32_gradient_bitwise(shape):
+    """The fused int8 step and the two-kernel step through an fp32 G accumulate every
+    element of G in the same order and share the epilogue arithmetic: identical bits."""
+    T, d_in, d_out = shape
+    p = make_problem(T, d_in, d_out, "i8", seed=77 + T)
+    a = run_gpu(p, 100)
+    b = run_gpu(p, 100, path="unfused", grad="f32")
+    for k in ("W", "m", "v", "m_scale", "v_scale"):
+        assert np.array_equal(a[k].view(np.uint8), b[k].view(np.uint8)), k
