@@ -694,13 +694,12 @@ __device__ __forceinline__ void epi_store_g(const Args &a, int p0, int q0, int s
 template <int BP, int BQ, int MK, int EPI>
 __global__ void __launch_bounds__(NT, 2) fused_kernel(GroupArgs g)
 {
-    using ML = Mainloop<BP, BQ, (MK == MK_I8 ? 3 : NSTAGE), (MK == MK_I8 ? 32 : TK128)>;
+    static_assert(MK != MK_I8, "int8 moments run in pipelined_i8_kernel");
+    using ML = Mainloop<BP, BQ, NSTAGE, TK128>;
     using EM = EpiMap<BP, BQ>;
-    constexpr int RED = (MK == MK_I8 && EPI == EPI_ADAMW) ? 2 * 4 * BQ * 4 : 0;
     constexpr int MAIN = ML::LDS_BYTES > EM::GS_BYTES ? ML::LDS_BYTES : EM::GS_BYTES;
-    __shared__ __attribute__((aligned(16))) unsigned char smem[MAIN + RED];
+    __shared__ __attribute__((aligned(16))) unsigned char smem[MAIN];
     float *Gs = reinterpret_cast<float *>(smem);
-    float *red = reinterpret_cast<float *>(smem + MAIN);
 
     const int tid = threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -713,35 +712,24 @@ __global__ void __launch_bounds__(NT, 2) fused_kernel(GroupArgs g)
     while (mi + 1 < g.n && t >= g.start[mi + 1]) ++mi;
     const Args a = g.a[mi];
     const int nbar = ML::nbar(a.T);
-    {
-        int tp, tq;
-        raster(t - g.start[mi], a.tiles_p, a.tiles_q, a.group_p, tp, tq);
-        const int p0 = tp * BP, q0 = tq * BQ;
-        if (wave < 4) {
-            ML ml;
-            ml.run(a, p0, q0, smem, wave, lane);
-            ml.template stage_g<EM::GP>(Gs, wave, lane);
-            lds_barrier();
-            if constexpr (MK == MK_I8 && EPI == EPI_ADAMW) lds_barrier();
-        } else if constexpr (EPI == EPI_ADAMW) {
-            if constexpr (MK == MK_I8) {
-                EpiAdamWI8<BP, BQ> ep;
-                ep.prefetch(a, p0, q0, s);
-                for (int i = 0; i < nbar; ++i) lds_barrier();
-                lds_barrier();
-                ep.run(a, p0, q0, s, Gs, red);
-            } else {
-                EpiAdamW<BP, BQ, MK> ep;
-                ep.prefetch(a, p0, q0, s);
-                for (int i = 0; i < nbar; ++i) lds_barrier();
-                lds_barrier();
-                ep.run(a, p0, q0, s, Gs);
-            }
-        } else {
-            for (int i = 0; i < nbar; ++i) lds_barrier();
-            lds_barrier();
-            epi_store_g<BP, BQ, EPI == EPI_STORE_F32>(a, p0, q0, s, Gs);
-        }
+    int tp, tq;
+    raster(t - g.start[mi], a.tiles_p, a.tiles_q, a.group_p, tp, tq);
+    const int p0 = tp * BP, q0 = tq * BQ;
+    if (wave < 4) {
+        ML ml;
+        ml.run(a, p0, q0, smem, wave, lane);
+        ml.template stage_g<EM::GP>(Gs, wave, lane);
+        lds_barrier();
+    } else if constexpr (EPI == EPI_ADAMW) {
+        EpiAdamW<BP, BQ, MK> ep;
+        ep.prefetch(a, p0, q0, s);
+        for (int i = 0; i < nbar; ++i) lds_barrier();
+        lds_barrier();
+        ep.run(a, p0, q0, s, Gs);
+    } else {
+        for (int i = 0; i < nbar; ++i) lds_barrier();
+        lds_barrier();
+        epi_store_g<BP, BQ, EPI == EPI_STORE_F32>(a, p0, q0, s, Gs);
     }
 }
 
