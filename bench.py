@@ -22,14 +22,16 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
 MFMA_BF16_PEAK_TFS = 2500.0    # dense bf16 MFMA, published
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2606_22932_amd", "csrc", "forge_kernels.hip")
+# Sources the fused kernel is compiled from (the traffic record below is tied to them).
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_22932_amd", "csrc", f)
+                  for f in ("forge_kernels.hip", "forge_device.h", "forge_internal.h")]
 COPY_BYTES = 1 << 30           # size of the calibration copy (--copy-calibration)
 
 # Measured HBM traffic of the fused kernel per launch, averaged over one step of a
 # workload: two rocprofv3 --pmc runs of `bench.py --steps 1 --warmup 0 --no-cpu-baseline
 # --no-unfused --copy-calibration` (FETCH_SIZE, then WRITE_SIZE), each counter scaled by
 # COPY_BYTES / (what it reads for the calibration copy).  Valid only for the kernel
-# source whose sha256 is recorded: after any change to it the figure is reported as null.
+# sources whose sha256 is recorded: after any change to them the figure is reported as null.
 TRAFFIC = {
     "sweep": {
         "source_sha256": "e8a0c54101a87726a11632ad0929ce72932d665a5f87f5818928956c11b250df",
@@ -93,9 +95,13 @@ def time_steps(launches, wl, fn, steps, warmup, step0):
 
 
 def source_sha256() -> str:
+    """sha256 over the fused kernel's source files, concatenated in KERNEL_SOURCES order."""
     import hashlib
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def measured_traffic(workload: str):
@@ -173,6 +179,9 @@ def main():
                     help="skip the measured HBM ceilings (a child process after the timed work)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run a plain 1 GiB device copy first (reference for counter scaling)")
+    ap.add_argument("--micro", action="store_true",
+                    help="instead of the sweep: the update-path microbenchmark (marginal cost of "
+                         "the fused update over the store-G control; q/o_proj shape, T=512 and 4096)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -187,6 +196,9 @@ def main():
     forge.lib()                                  # fails loudly if the HIP library is not built
     device = torch.device("cuda:0")
     torch.cuda.set_device(device)
+    if args.micro:
+        print(json.dumps(micro(device, args.steps, args.warmup)), flush=True)
+        return
     wl = synth.WORKLOADS[args.workload]
     if args.tokens is not None:
         if not 0 <= args.tokens <= wl.T:
@@ -300,6 +312,60 @@ def main():
             log(f"ceilings: {c}")
 
     print(json.dumps(out), flush=True)
+
+
+def micro(device, reps, warmup, d=4096, token_counts=(512, 4096)):
+    """Update-path microbenchmark (App. D): on the q/o_proj shape d x d, the average
+    duration of the store-G control (the same tile kernel with an epilogue that stores G
+    as bf16 instead of updating the optimizer state) and of the fused AdamW step (bf16 and
+    fp32 moments); the marginal cost of the update is their difference.  Also the
+    layer-level backward: dX = dY W alone and followed by the fused step.  Each figure is
+    `reps` back-to-back launches between two events on the launch stream, after `warmup`."""
+    import torch
+    from paper_2606_22932_amd import forge, synth
+    hp = dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.1)
+    stream = torch.cuda.current_stream()
+
+    def avg_us(fn):
+        for _ in range(warmup):
+            fn()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(stream)
+        for _ in range(reps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e3 / reps
+
+    rows = []
+    for T in token_counts:
+        log(f"micro: T={T}, {d}x{d}")
+        mat = synth.Matrix("qo", d, d, 2)
+        wl = dataclasses.replace(synth.WORKLOADS["o_proj"], T=T)
+        X, dY = synth.activations(T, mat, wl, 100, device=device)
+        W = synth.weight(mat, wl, device=device)
+        G = torch.empty((d, d), dtype=torch.bfloat16, device=device)
+        dX = torch.empty((T, d), dtype=torch.bfloat16, device=device)
+        mb, vb = synth.warm_moments(mat, wl, device=device, dtype=torch.bfloat16)
+        mf, vf = synth.warm_moments(mat, wl, device=device, dtype=torch.float32)
+        r = {"T": T, "shape": f"{d}x{d}"}
+        r["store_g_control_us"] = avg_us(lambda: forge.forge_wgrad(X, dY, G))
+        r["adamw_bf16_us"] = avg_us(lambda: forge.forge_linear_step(X, dY, W, mb, vb, step=100, **hp))
+        r["adamw_f32_us"] = avg_us(lambda: forge.forge_linear_step(X, dY, W, mf, vf, step=100, **hp))
+        r["input_grad_us"] = avg_us(lambda: forge.forge_input_grad(dY, W, dX))
+        r["backward_bf16_us"] = avg_us(lambda: forge.forge_linear_backward(X, dY, W, mb, vb, dX=dX, step=100,
+                                                                           **hp))
+        r["marginal_adamw_bf16_us"] = r["adamw_bf16_us"] - r["store_g_control_us"]
+        r["marginal_adamw_f32_us"] = r["adamw_f32_us"] - r["store_g_control_us"]
+        rows.append({k: (round(v, 2) if isinstance(v, float) else v) for k, v in r.items()})
+        log(f"micro: {rows[-1]}")
+        del X, dY, W, G, dX, mb, vb, mf, vf
+        torch.cuda.empty_cache()
+    return {"metric": "update-path microbenchmark: marginal cost of the fused AdamW update over the "
+                      "store-G control (us per launch)",
+            "unit": "us", "higher_is_better": False, "n_gpus": 1, "reps": reps, "warmup": warmup,
+            "data": "synthetic (seeded Gaussian X, dY, W, warm m, v)", "rows": rows}
 
 
 def hbm_ceilings():

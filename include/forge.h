@@ -139,6 +139,63 @@ FORGE_API forge_status forge_linear_step_grouped(const forge_matrix *mats, int32
                                        float eps, float weight_decay, int64_t step, void *stream);
 
 /*
+ * forge_input_grad -- the layer's input gradient dX = dY W (Algorithm 1, first line; the
+ * chain rule through Y = X W^T of Eq. fwd).
+ *
+ *   dY   bf16 [T, d_out]     upstream gradient (may be NULL when T, d_in or d_out is 0)
+ *   W    bf16 [d_out, d_in]  weight (may be NULL when T, d_in or d_out is 0)
+ *   dX   bf16 [T, d_in]      output, overwritten (may be NULL when T or d_in is 0)
+ *
+ * Products of bf16 inputs are accumulated in fp32 over d_out and rounded once to bf16
+ * (round-to-nearest-even).  d_out == 0 (with T, d_in > 0) fills dX with zeros.  Shape
+ * rules as in forge_linear_step; dX must not overlap dY or W (FORGE_ERR_ALIASING).
+ */
+FORGE_API forge_status forge_input_grad(const void *dY, const void *W, void *dX, int64_t T,
+                                        int64_t d_in, int64_t d_out, void *stream);
+
+/*
+ * forge_linear_backward -- the layer-level backward of FORGE (Sec. 2.2; Algorithm 1): the
+ * input gradient dX = dY W from the weight as it is before the step, then the fused step
+ * forge_linear_step, both enqueued on `stream` in that order.  Because the step overwrites
+ * W in place, dX has to be read off the pre-update weight (the ordering remark of App. A);
+ * stream order guarantees it.  Weights read by more than one backward path within a step
+ * (a tied embedding / LM head) must not use this call (same remark).
+ *
+ *   dX   bf16 [T, d_in], output (may be NULL when T or d_in is 0); other arguments as in
+ *        forge_linear_step.
+ *
+ * Identical to forge_linear_backward_grouped with n == 1 (validation order included):
+ * W, m, v end bit-identical to forge_linear_step's, dX bit-identical to forge_input_grad's
+ * on the pre-update W.
+ */
+FORGE_API forge_status forge_linear_backward(const void *X, const void *dY, void *W, void *m, void *v,
+                                             float *m_scale, float *v_scale, void *dX, int64_t T,
+                                             int64_t d_in, int64_t d_out, int32_t moment_dtype,
+                                             float lr, float beta1, float beta2, float eps,
+                                             float weight_decay, int64_t step, void *stream);
+
+/*
+ * forge_linear_backward_grouped -- the layer-level backward of n projections of one input
+ * (for example q, k and v, or an MLP's gate and up): that input's gradient is the sum of
+ * their contributions, dX = sum_i dY_i W_i, formed in one launch from the pre-update
+ * weights (fp32 accumulation over the concatenated d_out axes, one rounding to bf16), then
+ * forge_linear_step_grouped on the n matrices, in stream order.
+ *
+ *   mats   n descriptors as for forge_linear_step_grouped; all must have the same d_in
+ *          (else FORGE_ERR_INVALID_SHAPE); members with d_out == 0 add nothing to dX
+ *   dX     bf16 [T, d_in], output (may be NULL when T or d_in is 0)
+ *
+ * Validation, in this order: the moment dtype; mats and n; equal d_in; then exactly as
+ * forge_linear_step_grouped (each matrix, hyper-parameters, aliasing); then dX (NULL:
+ * FORGE_ERR_NULL_POINTER, misaligned: FORGE_ERR_MISALIGNED, overlapping any member's X, dY
+ * or state tensors: FORGE_ERR_ALIASING); the device.
+ */
+FORGE_API forge_status forge_linear_backward_grouped(const forge_matrix *mats, int32_t n, int64_t T,
+                                                     void *dX, int32_t moment_dtype, float lr,
+                                                     float beta1, float beta2, float eps,
+                                                     float weight_decay, int64_t step, void *stream);
+
+/*
  * forge_wgrad -- the weight-gradient GEMM alone, storing G = dY^T X (Eq. wgrad) to
  * `G` [d_out, d_in] in `grad_dtype` (bf16 with round-to-nearest-even, or fp32).  This is
  * the first kernel of the two-kernel comparison path and the store-G control of App. D.

@@ -53,6 +53,10 @@ def _load():
             lib.forge_oracle_f64_to_bf16.restype = ctypes.c_uint16
             lib.forge_oracle_wgrad.argtypes = [P, P, I64, I64, I64, P]
             lib.forge_oracle_wgrad.restype = None
+            lib.forge_oracle_f64_to_bf16_array.argtypes = [P, I64, P]
+            lib.forge_oracle_f64_to_bf16_array.restype = None
+            lib.forge_oracle_input_grad.argtypes = [P, P, I64, I64, I64, P]
+            lib.forge_oracle_input_grad.restype = None
             lib.forge_oracle_quantize_i8.argtypes = [P, I64, I64, I32, P, P]
             lib.forge_oracle_quantize_i8.restype = None
             lib.forge_oracle_adamw.argtypes = [P, P, P, P, P, P, I64, I64, I32, F32, F32, F32, F32,
@@ -90,12 +94,9 @@ def bf16_bits_to_f64(bits: np.ndarray) -> np.ndarray:
 
 def f64_to_bf16_bits(x) -> np.ndarray:
     """fp64 -> bf16 bit patterns, round to nearest even in one step (the oracle's C routine)."""
-    lib = _load()
-    x = np.asarray(x, dtype=np.float64)
+    x = np.ascontiguousarray(np.asarray(x, dtype=np.float64))
     out = np.empty(x.shape, dtype=np.uint16)
-    flat, of = x.reshape(-1), out.reshape(-1)
-    for i in range(flat.size):
-        of[i] = lib.forge_oracle_f64_to_bf16(float(flat[i]))
+    _load().forge_oracle_f64_to_bf16_array(_ptr(x), x.size, _ptr(out))
     return out
 
 
@@ -111,6 +112,19 @@ def wgrad(X: np.ndarray, dY: np.ndarray) -> np.ndarray:
     G = np.empty((d_out, d_in), dtype=np.float64)
     _load().forge_oracle_wgrad(_ptr(X), _ptr(dY), T, d_in, d_out, _ptr(G))
     return G
+
+
+def input_grad(dY: np.ndarray, W: np.ndarray) -> np.ndarray:
+    """dX = dY W in fp64 (Algorithm 1, first line): dY bf16 bits [T, d_out], W bf16 bits
+    [d_out, d_in] -> [T, d_in].  The layer-level backward forms it from the pre-update W."""
+    dY, W = _c(dY, np.uint16), _c(W, np.uint16)
+    T, d_out = dY.shape
+    d_out2, d_in = W.shape
+    if d_out != d_out2:
+        raise ValueError("dY and W disagree on d_out")
+    dX = np.empty((T, d_in), dtype=np.float64)
+    _load().forge_oracle_input_grad(_ptr(dY), _ptr(W), T, d_in, d_out, _ptr(dX))
+    return dX
 
 
 def quantize_i8(x: np.ndarray, second_moment: bool):
@@ -175,4 +189,13 @@ def linear_step(X, dY, W, m, v, **kw):
     G = wgrad(X, dY)
     out = adamw(G, W, m, v, **kw)
     out["G"] = G
+    return out
+
+
+def linear_backward(X, dY, W, m, v, **kw):
+    """The layer-level backward: dX = dY W from the weight before the step (fp64, key
+    ``dX``), then ``linear_step``.  Sec. 2.2 and the ordering remark of App. A."""
+    dX = input_grad(dY, W)
+    out = linear_step(X, dY, W, m, v, **kw)
+    out["dX"] = dX
     return out

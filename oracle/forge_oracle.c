@@ -28,6 +28,11 @@
  *
  * Hyper-parameters arrive as the fp32 values the GPU receives; they are promoted
  * to fp64 here, so lr = 1e-3 means (double)(float)1e-3.
+ *
+ * The layer-level backward adds one more quantity, computed before the update:
+ *   0. the input gradient dX = dY W from the pre-update weight (Algorithm 1, first
+ *      line; the ordering remark of App. A), dX[t][q] = sum_p dY[t][p] * W[p][q],
+ *      summed in order p = 0..d_out-1, in fp64.
  */
 #include <math.h>
 #include <stdint.h>
@@ -99,6 +104,40 @@ void forge_oracle_wgrad(const uint16_t *X, const uint16_t *dY, int64_t T,
         }
     }
     free(Xd);
+}
+
+/* Elementwise forge_oracle_f64_to_bf16 over n values. */
+void forge_oracle_f64_to_bf16_array(const double *x, int64_t n, uint16_t *out)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i) out[i] = forge_oracle_f64_to_bf16(x[i]);
+}
+
+/* ------------------------------------------------------------- 0. input gradient */
+
+/*
+ * dX[t*d_in + q] = sum_p dY[t*d_out + p] * W[p*d_in + q]   (chain rule through
+ * Y = X W^T, Eq. fwd; Algorithm 1, first line).  dY: bf16 [T, d_out], W: bf16
+ * [d_out, d_in], both row-major.  dX: fp64 [T, d_in].  Every element's sum runs over
+ * p = 0..d_out-1 in order; d_out == 0 gives zeros.
+ */
+void forge_oracle_input_grad(const uint16_t *dY, const uint16_t *W, int64_t T, int64_t d_in,
+                             int64_t d_out, double *dX)
+{
+    double *Wd = (double *)malloc(sizeof(double) * (size_t)(d_out * d_in > 0 ? d_out * d_in : 1));
+    for (int64_t i = 0; i < d_out * d_in; ++i) Wd[i] = forge_oracle_bf16_to_f64(W[i]);
+
+#pragma omp parallel for schedule(dynamic, 4)
+    for (int64_t t = 0; t < T; ++t) {
+        double *row = dX + t * d_in;
+        for (int64_t q = 0; q < d_in; ++q) row[q] = 0.0;
+        for (int64_t p = 0; p < d_out; ++p) {
+            double a = forge_oracle_bf16_to_f64(dY[t * d_out + p]);
+            const double *wr = Wd + p * d_in;
+            for (int64_t q = 0; q < d_in; ++q) row[q] += a * wr[q];
+        }
+    }
+    free(Wd);
 }
 
 /* ------------------------------------------------------------- int8 quantizer */

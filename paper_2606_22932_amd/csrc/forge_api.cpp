@@ -176,6 +176,61 @@ Args base_args(const void *X, const void *dY, int64_t T, int64_t d_in, int64_t d
     return a;
 }
 
+// The validated launch arguments of a grouped step (empty matrices dropped).
+struct GroupPlan {
+    StateSet st[FORGE_MAX_GROUP];
+    int live[FORGE_MAX_GROUP];
+    int nlive = 0;
+    Args args[FORGE_MAX_GROUP];
+};
+
+// Validation of forge_linear_step_grouped after the dtype, mats and n checks: each matrix,
+// then (if any is non-empty) the hyper-parameters and the aliasing rules.
+forge_status plan_group(const forge_matrix *mats, int32_t n, int64_t T, int32_t md, float lr,
+                        float beta1, float beta2, float eps, float weight_decay, int64_t step,
+                        GroupPlan &g)
+{
+    forge_status s;
+    g.nlive = 0;
+    for (int i = 0; i < n; ++i) {
+        const forge_matrix &x = mats[i];
+        bool empty = false;
+        if ((s = check_shape(T, x.d_in, x.d_out, empty)) != FORGE_OK) return s;
+        if (empty) continue;
+        if ((s = check_inputs(x.X, x.dY, T, x.d_in, x.d_out)) != FORGE_OK) return s;
+        if ((s = check_state(x.W, x.m, x.v, x.m_scale, x.v_scale, x.d_in, x.d_out, md, g.st[g.nlive])) !=
+            FORGE_OK)
+            return s;
+        g.live[g.nlive++] = i;
+    }
+    if (g.nlive == 0) return FORGE_OK;
+    if ((s = check_hyper(lr, beta1, beta2, eps, weight_decay, step)) != FORGE_OK) return s;
+    for (int a = 0; a < g.nlive; ++a) {
+        for (int b = 0; b < g.nlive; ++b) {
+            const forge_matrix &y = mats[g.live[b]];
+            if (T > 0 && (!disjoint_from(g.st[a], range_of(y.X, 2 * T * y.d_in)) ||
+                          !disjoint_from(g.st[a], range_of(y.dY, 2 * T * y.d_out))))
+                return FORGE_ERR_ALIASING;
+            if (b > a)
+                for (int k = 0; k < g.st[b].n; ++k)
+                    if (!disjoint_from(g.st[a], g.st[b].r[k])) return FORGE_ERR_ALIASING;
+        }
+    }
+    const Hyper h = make_hyper(lr, beta1, beta2, eps, weight_decay, step);
+    for (int k = 0; k < g.nlive; ++k) {
+        const forge_matrix &x = mats[g.live[k]];
+        Args &a = g.args[k];
+        a = base_args(x.X, x.dY, T, x.d_in, x.d_out);
+        a.W = static_cast<uint16_t *>(x.W);
+        a.m = x.m;
+        a.v = x.v;
+        a.ms = x.m_scale;
+        a.vs = x.v_scale;
+        a.h = h;
+    }
+    return FORGE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -248,48 +303,85 @@ forge_status forge_linear_step_grouped(const forge_matrix *mats, int32_t n, int6
     if ((s = check_dtype_moment(md)) != FORGE_OK) return s;
     if (!mats) return FORGE_ERR_NULL_POINTER;
     if (n < 1 || n > FORGE_MAX_GROUP) return FORGE_ERR_INVALID_SHAPE;
-    StateSet st[FORGE_MAX_GROUP];
-    int live[FORGE_MAX_GROUP];
-    int nlive = 0;
-    for (int i = 0; i < n; ++i) {
-        const forge_matrix &x = mats[i];
-        bool empty = false;
-        if ((s = check_shape(T, x.d_in, x.d_out, empty)) != FORGE_OK) return s;
-        if (empty) continue;
-        if ((s = check_inputs(x.X, x.dY, T, x.d_in, x.d_out)) != FORGE_OK) return s;
-        if ((s = check_state(x.W, x.m, x.v, x.m_scale, x.v_scale, x.d_in, x.d_out, md, st[nlive])) != FORGE_OK)
-            return s;
-        live[nlive++] = i;
-    }
-    if (nlive == 0) return FORGE_OK;
-    if ((s = check_hyper(lr, beta1, beta2, eps, weight_decay, step)) != FORGE_OK) return s;
-    for (int a = 0; a < nlive; ++a) {
-        for (int b = 0; b < nlive; ++b) {
-            const forge_matrix &y = mats[live[b]];
-            if (T > 0 && (!disjoint_from(st[a], range_of(y.X, 2 * T * y.d_in)) ||
-                          !disjoint_from(st[a], range_of(y.dY, 2 * T * y.d_out))))
+    GroupPlan g;
+    if ((s = plan_group(mats, n, T, md, lr, beta1, beta2, eps, weight_decay, step, g)) != FORGE_OK) return s;
+    if (g.nlive == 0) return FORGE_OK;
+    if ((s = check_device()) != FORGE_OK) return s;
+    return from_hip(forge_impl::launch_fused_group(g.args, g.nlive, md, static_cast<hipStream_t>(stream)));
+}
+
+forge_status forge_input_grad(const void *dY, const void *W, void *dX, int64_t T, int64_t d_in,
+                              int64_t d_out, void *stream)
+{
+    forge_status s;
+    bool empty = false;
+    if ((s = check_shape(T, d_in, d_out, empty)) != FORGE_OK) return s;
+    if (T == 0 || d_in == 0) return FORGE_OK;
+    if (!dX) return FORGE_ERR_NULL_POINTER;
+    if (d_out > 0 && (!dY || !W)) return FORGE_ERR_NULL_POINTER;
+    if (!aligned16(dX)) return FORGE_ERR_MISALIGNED;
+    if (d_out > 0 && (!aligned16(dY) || !aligned16(W))) return FORGE_ERR_MISALIGNED;
+    const Range rdx = range_of(dX, 2 * T * d_in);
+    if (d_out > 0 && (overlap(rdx, range_of(dY, 2 * T * d_out)) || overlap(rdx, range_of(W, 2 * d_in * d_out))))
+        return FORGE_ERR_ALIASING;
+    if ((s = check_device()) != FORGE_OK) return s;
+    const forge_impl::DxSeg seg{static_cast<const uint16_t *>(dY), static_cast<const uint16_t *>(W),
+                                static_cast<int>(d_out)};
+    return from_hip(forge_impl::launch_dx(&seg, d_out > 0 ? 1 : 0, static_cast<uint16_t *>(dX),
+                                          static_cast<int>(T), static_cast<int>(d_in),
+                                          static_cast<hipStream_t>(stream)));
+}
+
+forge_status forge_linear_backward_grouped(const forge_matrix *mats, int32_t n, int64_t T, void *dX,
+                                           int32_t md, float lr, float beta1, float beta2, float eps,
+                                           float weight_decay, int64_t step, void *stream)
+{
+    forge_status s;
+    if ((s = check_dtype_moment(md)) != FORGE_OK) return s;
+    if (!mats) return FORGE_ERR_NULL_POINTER;
+    if (n < 1 || n > FORGE_MAX_GROUP) return FORGE_ERR_INVALID_SHAPE;
+    const int64_t d_in = mats[0].d_in;
+    for (int i = 1; i < n; ++i)
+        if (mats[i].d_in != d_in) return FORGE_ERR_INVALID_SHAPE;
+    GroupPlan g;
+    if ((s = plan_group(mats, n, T, md, lr, beta1, beta2, eps, weight_decay, step, g)) != FORGE_OK) return s;
+    const bool has_dx = T > 0 && d_in > 0;
+    if (has_dx) {
+        if (!dX) return FORGE_ERR_NULL_POINTER;
+        if (!aligned16(dX)) return FORGE_ERR_MISALIGNED;
+        const Range rdx = range_of(dX, 2 * T * d_in);
+        for (int k = 0; k < g.nlive; ++k) {
+            const forge_matrix &x = mats[g.live[k]];
+            if (!disjoint_from(g.st[k], rdx) || overlap(rdx, range_of(x.X, 2 * T * x.d_in)) ||
+                overlap(rdx, range_of(x.dY, 2 * T * x.d_out)))
                 return FORGE_ERR_ALIASING;
-            if (b > a)
-                for (int k = 0; k < st[b].n; ++k)
-                    if (!disjoint_from(st[a], st[b].r[k])) return FORGE_ERR_ALIASING;
         }
     }
+    if (!has_dx && g.nlive == 0) return FORGE_OK;
     if ((s = check_device()) != FORGE_OK) return s;
-
-    const Hyper h = make_hyper(lr, beta1, beta2, eps, weight_decay, step);
-    Args args[FORGE_MAX_GROUP];
-    for (int k = 0; k < nlive; ++k) {
-        const forge_matrix &x = mats[live[k]];
-        Args &a = args[k];
-        a = base_args(x.X, x.dY, T, x.d_in, x.d_out);
-        a.W = static_cast<uint16_t *>(x.W);
-        a.m = x.m;
-        a.v = x.v;
-        a.ms = x.m_scale;
-        a.vs = x.v_scale;
-        a.h = h;
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    if (has_dx) {
+        // dX from the weights as they are before this step (the fused launch below, later in
+        // stream order, overwrites them).  Members with d_out == 0 add nothing to the sum.
+        forge_impl::DxSeg seg[FORGE_MAX_GROUP];
+        for (int k = 0; k < g.nlive; ++k)
+            seg[k] = forge_impl::DxSeg{g.args[k].dY, g.args[k].W, g.args[k].d_out};
+        if ((s = from_hip(forge_impl::launch_dx(seg, g.nlive, static_cast<uint16_t *>(dX), static_cast<int>(T),
+                                                static_cast<int>(d_in), st))) != FORGE_OK)
+            return s;
     }
-    return from_hip(forge_impl::launch_fused_group(args, nlive, md, static_cast<hipStream_t>(stream)));
+    if (g.nlive == 0) return FORGE_OK;
+    return from_hip(forge_impl::launch_fused_group(g.args, g.nlive, md, st));
+}
+
+forge_status forge_linear_backward(const void *X, const void *dY, void *W, void *m, void *v,
+                                   float *m_scale, float *v_scale, void *dX, int64_t T, int64_t d_in,
+                                   int64_t d_out, int32_t md, float lr, float beta1, float beta2,
+                                   float eps, float weight_decay, int64_t step, void *stream)
+{
+    const forge_matrix x{X, dY, W, m, v, m_scale, v_scale, d_in, d_out};
+    return forge_linear_backward_grouped(&x, 1, T, dX, md, lr, beta1, beta2, eps, weight_decay, step,
+                                         stream);
 }
 
 forge_status forge_wgrad(const void *X, const void *dY, void *G, int64_t T, int64_t d_in,

@@ -43,6 +43,25 @@ struct GroupArgs {
     int n;
 };
 
+// One term dY_s W_s of the input gradient (forge_dx.hip): dY_s bf16 [T, d_out],
+// W_s bf16 [d_out, d_in]; d_out > 0.
+struct DxSeg {
+    const uint16_t *dY;
+    const uint16_t *W;
+    int d_out;
+};
+
+// A launch of the input-gradient GEMM dX = sum_s dY_s W_s (kernel argument).
+struct DxArgs {
+    DxSeg s[MAX_GROUP];
+    int n;                 // segments
+    int nch;               // K chunks over all segments
+    uint16_t *dX;          // bf16 [T, d_in]
+    int T, d_in;
+    int tiles_t, tiles_q;  // tile grid (along T, along d_in)
+    int group_t;           // raster group height in tiles
+};
+
 enum MomentKind { MK_F32 = 0, MK_BF16 = 1, MK_I8 = 2 };
 enum EpiKind { EPI_ADAMW = 0, EPI_STORE_BF16 = 1, EPI_STORE_F32 = 2 };
 
@@ -57,5 +76,11 @@ hipError_t launch_fused(const Args &a, int moment_kind, hipStream_t stream);
 hipError_t launch_fused_group(const Args *a, int n, int moment_kind, hipStream_t stream);
 hipError_t launch_wgrad(const Args &a, int grad_f32, hipStream_t stream);
 hipError_t launch_adamw(const Args &a, int moment_kind, int grad_f32, hipStream_t stream);
+// dX = sum of dY_s W_s over n segments (0 <= n <= MAX_GROUP, none with d_out == 0; n == 0
+// writes zeros).  No launch when T == 0 or d_in == 0.
+hipError_t launch_dx(const DxSeg *s, int n, uint16_t *dX, int T, int d_in, hipStream_t stream);
+
+// Compute units of the current device (cached per device ordinal; 256 if unknown).
+int device_cu_count();
 
 }  // namespace forge_impl

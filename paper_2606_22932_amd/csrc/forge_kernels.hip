@@ -16,19 +16,11 @@
 // The two-kernel comparison path reuses the same pieces: the store-G GEMM runs the same
 // mainloop with an epilogue that writes G, and the stand-alone optimizer stages a tile
 // of a materialised G into LDS and runs the same epilogue code.
-#include "forge_internal.h"
+#include "forge_device.h"
 
 #include <mutex>
 
 namespace forge_impl {
-
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
-typedef short v4i16_t __attribute__((ext_vector_type(4)));
 
 #ifndef FORGE_TK
 #define FORGE_TK 32
@@ -43,6 +35,9 @@ typedef short v4i16_t __attribute__((ext_vector_type(4)));
 #define FORGE_NSW_I8P 8
 #endif
 constexpr int NS_I8P = FORGE_NS_I8P;
+#ifndef FORGE_SCHED_SPLIT         // sched_barrier between the two MFMA steps of a chunk
+#define FORGE_SCHED_SPLIT 1
+#endif
 #ifndef FORGE_GROUP_P             // tile rows walked together by the raster (0: by shape)
 #define FORGE_GROUP_P 0
 #endif
@@ -51,10 +46,6 @@ constexpr int NSTAGE = FORGE_NS;  // LDS ring depth (chunks) of the 128x128 main
 constexpr int NROLE = 256;      // threads per role (4 waves)
 constexpr int NT = 2 * NROLE;   // threads per fused workgroup
 constexpr int I8_BLOCK = 256;   // rows of d_out sharing one int8 scale
-// Buffer offset of a DMA piece that must read zero.  Tensors hold fewer than 2^31
-// elements and d_in, d_out are multiples of 8, so a chunk spans at most 2^32 - 16 bytes:
-// this offset is past the end of every chunk's buffer.
-constexpr uint32_t OOR_OFFSET = 0xFFFFFFF0u;
 
 // Tile shapes: (rows along d_out) x (cols along d_in).  int8 tiles are exactly one scale
 // block tall so that the block absmax closes inside the workgroup.
@@ -62,31 +53,6 @@ constexpr int BP_F = 128, BQ_F = 128;
 constexpr int BP_I8 = 256, BQ_I8 = 64;
 
 // ------------------------------------------------------------------------ small helpers
-
-__device__ __forceinline__ void lds_barrier()
-{
-    // Wait for this wave's LDS traffic only, then barrier: outstanding global loads (the
-    // stream waves' prefetch) stay in flight across it.
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-}
-
-__device__ __forceinline__ float bf_lo(uint32_t u) { return __uint_as_float(u << 16); }
-__device__ __forceinline__ float bf_hi(uint32_t u) { return __uint_as_float(u & 0xFFFF0000u); }
-
-__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi)
-{
-    bf16x2_t r = {(__bf16)lo, (__bf16)hi};   // v_cvt_pk_bf16_f32: round to nearest even
-    return __builtin_bit_cast(uint32_t, r);
-}
-
-template <typename T> __device__ __forceinline__ T ld_nt(const void *p)
-{
-    return __builtin_nontemporal_load(reinterpret_cast<const T *>(p));
-}
-template <typename T> __device__ __forceinline__ void st_nt(void *p, T v)
-{
-    __builtin_nontemporal_store(v, reinterpret_cast<T *>(p));
-}
 
 // One AdamW element (Algorithm 1): state update, then the bias-corrected decoupled
 // weight update.  rv1 = sqrt(v1) is returned as well (the int8 path stores it).
@@ -99,34 +65,6 @@ __device__ __forceinline__ void adamw_elem(float g, float w, float m, float v, c
     float den = __builtin_fmaf(rv1, h.inv_sqrt_bc2, h.eps);        // sqrt(vhat) + eps
     float upd = (m1 * h.lr_bc1) * __builtin_amdgcn_rcpf(den);       // lr * mhat / den
     w1 = __builtin_fmaf(h.wdf, w, -upd);
-}
-
-// Workgroups are dispatched round-robin over the 8 XCDs (each with its own L2): give
-// each XCD a contiguous run of the ntiles tiles of a launch.
-__device__ __forceinline__ int xcd_remap(int bid, int ntiles)
-{
-    const int k = ntiles >> 3, r = ntiles & 7;
-    const int x = bid & 7, s = bid >> 3;
-    return (x < r) ? x * (k + 1) + s : r * (k + 1) + (x - r) * k + s;
-}
-
-// Tile t of one matrix in groups of `group_p` tile rows, so that concurrently resident
-// tiles share their dY row slabs and X column slabs.
-__device__ __forceinline__ void raster(int t, int tiles_p, int tiles_q, int group_p, int &tp, int &tq)
-{
-    const int per_group = group_p * tiles_q;
-    const int g = t / per_group;
-    const int first = g * group_p;
-    const int gsz = min(group_p, tiles_p - first);
-    const int within = t - g * per_group;
-    tp = first + within % gsz;
-    tq = within / gsz;
-}
-
-__device__ __forceinline__ void tile_of(int bid, int ntiles, int tiles_p, int tiles_q,
-                                        int group_p, int &tp, int &tq)
-{
-    raster(xcd_remap(bid, ntiles), tiles_p, tiles_q, group_p, tp, tq);
 }
 
 // ------------------------------------------------------------------------ mainloop
@@ -274,6 +212,9 @@ struct Mainloop {
             for (int ip = 0; ip < 2; ++ip)
                 acc[iq][ip] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
                     cat(fa[0][iq][0], fa[0][iq][1]), cat(fb[0][ip][0], fb[0][ip][1]), acc[iq][ip], 0, 0, 0);
+#if FORGE_SCHED_SPLIT
+        __builtin_amdgcn_sched_barrier(0);   // keep the first step's MFMAs ahead of the next wait
+#endif
         asm volatile("s_waitcnt lgkmcnt(0)"
                      : "+v"(fa[1][0][0]), "+v"(fa[1][0][1]), "+v"(fa[1][1][0]), "+v"(fa[1][1][1]),
                        "+v"(fb[1][0][0]), "+v"(fb[1][0][1]), "+v"(fb[1][1][0]), "+v"(fb[1][1][1]));
@@ -1190,8 +1131,7 @@ static hipError_t launch_group(const Args *a, int n, hipStream_t st)
     return hipGetLastError();
 }
 
-// Compute units of the current device (cached per device ordinal).
-static int cu_count()
+int device_cu_count()
 {
     static std::mutex mu;
     static int known[64] = {0};
@@ -1223,7 +1163,7 @@ static hipError_t launch_i8_pipelined(const Args *a, int n, hipStream_t st)
     }
     const int total = g.start[n];
     if (total == 0) return hipSuccess;
-    const int ncu = cu_count();
+    const int ncu = device_cu_count();
     const int grid = total < ncu ? total : ncu;
     hipLaunchKernelGGL(pipelined_i8_kernel, dim3(grid), dim3(NT_I8P), 0, st, g);
     return hipGetLastError();

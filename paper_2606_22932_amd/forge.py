@@ -50,6 +50,11 @@ _SIGS = {
     "forge_linear_step": [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I32, _F, _F, _F, _F, _F, _I64, _P],
     "forge_linear_step_grouped": [ctypes.POINTER(forge_matrix), _I32, _I64, _I32, _F, _F, _F, _F, _F,
                                   _I64, _P],
+    "forge_input_grad": [_P, _P, _P, _I64, _I64, _I64, _P],
+    "forge_linear_backward": [_P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I32, _F, _F, _F, _F, _F,
+                              _I64, _P],
+    "forge_linear_backward_grouped": [ctypes.POINTER(forge_matrix), _I32, _I64, _P, _I32, _F, _F, _F, _F,
+                                      _F, _I64, _P],
     "forge_wgrad": [_P, _P, _P, _I64, _I64, _I64, _I32, _P],
     "forge_adamw": [_P, _I32, _P, _P, _P, _P, _P, _I64, _I64, _I32, _F, _F, _F, _F, _F, _I64, _P],
     "forge_linear_step_unfused": [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I32, _F, _F, _F, _F,
@@ -160,12 +165,8 @@ def forge_linear_step(X, dY, W, m, v, m_scale=None, v_scale=None, *, lr, beta1, 
     _check(st, "forge_linear_step")
 
 
-def forge_linear_step_grouped(mats, *, lr, beta1, beta2, eps, weight_decay, step, stream=None):
-    """The fused step on several independent matrices in one launch.
-
-    ``mats``: sequence of ``(X, dY, W, m, v)`` or ``(X, dY, W, m, v, m_scale, v_scale)``
-    tuples sharing the token count T and the moment dtype (at most FORGE_MAX_GROUP).
-    """
+def _group(mats):
+    """ctypes array of forge_matrix for (X, dY, W, m, v[, m_scale, v_scale]) tuples, T, dtype code."""
     mats = [tuple(x) + (None,) * (7 - len(x)) for x in mats]
     if not mats:
         raise ValueError("empty group")
@@ -182,9 +183,64 @@ def forge_linear_step_grouped(mats, *, lr, beta1, beta2, eps, weight_decay, step
         arr[i] = forge_matrix(X.data_ptr(), dY.data_ptr(), W.data_ptr(), m.data_ptr(), v.data_ptr(),
                               None if ms is None else ms.data_ptr(), None if vs is None else vs.data_ptr(),
                               d_in, d_out)
-    st = lib().forge_linear_step_grouped(arr, len(mats), T, code, lr, beta1, beta2, eps, weight_decay,
-                                         int(step), _stream(stream, mats[0][2]))
+    return arr, len(mats), T, code, mats[0][2]
+
+
+def forge_linear_step_grouped(mats, *, lr, beta1, beta2, eps, weight_decay, step, stream=None):
+    """The fused step on several independent matrices in one launch.
+
+    ``mats``: sequence of ``(X, dY, W, m, v)`` or ``(X, dY, W, m, v, m_scale, v_scale)``
+    tuples sharing the token count T and the moment dtype (at most FORGE_MAX_GROUP).
+    """
+    arr, n, T, code, ref = _group(mats)
+    st = lib().forge_linear_step_grouped(arr, n, T, code, lr, beta1, beta2, eps, weight_decay,
+                                         int(step), _stream(stream, ref))
     _check(st, "forge_linear_step_grouped")
+
+
+def _dx(dX, T, d_in):
+    import torch
+    _dev(dX)
+    if dX.dtype != torch.bfloat16 or tuple(dX.shape) != (T, d_in):
+        raise ValueError(f"dX must be bfloat16 [{T}, {d_in}], got {dX.dtype} {tuple(dX.shape)}")
+
+
+def forge_input_grad(dY, W, dX, *, stream=None):
+    """dX = dY W (bf16 out, fp32 accumulation): the layer's input gradient."""
+    import torch
+    _dev(dY, W)
+    if dY.dtype != torch.bfloat16 or W.dtype != torch.bfloat16:
+        raise TypeError("dY and W must be bfloat16")
+    T, d_out = dY.shape
+    if W.shape[0] != d_out:
+        raise ValueError(f"shape mismatch: dY {tuple(dY.shape)}, W {tuple(W.shape)}")
+    d_in = W.shape[1]
+    _dx(dX, T, d_in)
+    st = lib().forge_input_grad(_ptr(dY), _ptr(W), _ptr(dX), T, d_in, d_out, _stream(stream, dX))
+    _check(st, "forge_input_grad")
+
+
+def forge_linear_backward(X, dY, W, m, v, m_scale=None, v_scale=None, *, dX, lr, beta1, beta2, eps,
+                          weight_decay, step, stream=None):
+    """The layer-level backward: dX = dY W from the pre-update W, then the fused step."""
+    _dev(X, dY, W, m, v, m_scale, v_scale)
+    T, d_in, d_out = _shapes(X, dY, W)
+    _dx(dX, T, d_in)
+    st = lib().forge_linear_backward(_ptr(X), _ptr(dY), _ptr(W), _ptr(m), _ptr(v), _ptr(m_scale),
+                                     _ptr(v_scale), _ptr(dX), T, d_in, d_out, _moment_code(m), lr, beta1,
+                                     beta2, eps, weight_decay, int(step), _stream(stream, W))
+    _check(st, "forge_linear_backward")
+
+
+def forge_linear_backward_grouped(mats, *, dX, lr, beta1, beta2, eps, weight_decay, step, stream=None):
+    """Backward of several projections of one input: dX = sum_i dY_i W_i (pre-update
+    weights, one launch), then the grouped fused step.  ``mats`` as for
+    ``forge_linear_step_grouped``; all share d_in."""
+    arr, n, T, code, ref = _group(mats)
+    _dx(dX, T, arr[0].d_in)
+    st = lib().forge_linear_backward_grouped(arr, n, T, _ptr(dX), code, lr, beta1, beta2, eps,
+                                             weight_decay, int(step), _stream(stream, ref))
+    _check(st, "forge_linear_backward_grouped")
 
 
 def forge_wgrad(X, dY, G, *, stream=None):

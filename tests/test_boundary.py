@@ -214,3 +214,97 @@ def test_group_valid_arguments_reach_the_device_check():
     m0 = _mat(0)
     assert call_group([m0, _mat(1, X=m0.X), _mat(2, X=m0.X)]) == NODEV
     assert call_group([_mat(0), _mat(1, d_in=0)], T=0) == NODEV
+
+
+# ----------------------------------------------------------------------------- input gradient and backward
+
+DX = 60 * GiB   # fake dX, apart from every other fake tensor
+
+
+def call_input_grad(T=64, d_in=128, d_out=256, dY=BASE["dY"], W=BASE["W"], dX=DX):
+    return lib().forge_input_grad(dY, W, dX, T, d_in, d_out, None)
+
+
+def call_backward(T=64, d_in=128, d_out=256, md=BF16, dX=DX, **over):
+    a = dict(BASE)
+    a.update({k: v for k, v in over.items() if k in a})
+    hp = dict(HP)
+    hp.update({k: v for k, v in over.items() if k in hp})
+    return lib().forge_linear_backward(a["X"], a["dY"], a["W"], a["m"], a["v"], a["ms"], a["vs"], dX, T, d_in,
+                                       d_out, md, hp["lr"], hp["beta1"], hp["beta2"], hp["eps"], hp["wd"],
+                                       hp["step"], None)
+
+
+def call_backward_group(mats, T=64, md=BF16, n=None, dX=DX, **over):
+    hp = dict(HP)
+    hp.update(over)
+    arr = (forge.forge_matrix * max(1, len(mats)))(*mats)
+    return lib().forge_linear_backward_grouped(arr, len(mats) if n is None else n, T, dX, md, hp["lr"],
+                                               hp["beta1"], hp["beta2"], hp["eps"], hp["wd"], hp["step"], None)
+
+
+def test_input_grad_errors():
+    assert call_input_grad(T=-1) == SHAPE
+    assert call_input_grad(d_in=12) == UNSUP
+    assert call_input_grad(d_out=(1 << 31) // 64 + 8) == UNSUP           # dY past 2^31 elements
+    assert call_input_grad(dX=0) == NULLP
+    assert call_input_grad(dY=0) == NULLP
+    assert call_input_grad(W=0) == NULLP
+    assert call_input_grad(dX=DX + 8) == MISAL
+    assert call_input_grad(W=BASE["W"] + 2) == MISAL
+    assert call_input_grad(dX=BASE["dY"] + 64) == ALIAS
+    assert call_input_grad(dX=BASE["W"] - 16) == ALIAS                   # dX's tail runs into W
+
+
+def test_input_grad_empty_is_a_noop():
+    # nothing to write: no pointer is read
+    assert call_input_grad(T=0, dY=0, W=0, dX=0) == OK
+    assert call_input_grad(d_in=0, dY=0, W=0, dX=0) == OK
+
+
+@pytest.mark.skipif(_gpu_visible(), reason="on a GPU machine a valid call would launch on fake pointers")
+def test_input_grad_valid_arguments_reach_the_device_check():
+    assert call_input_grad() == NODEV
+    assert call_input_grad(d_out=0, dY=0, W=0) == NODEV                  # zero fill of dX
+
+
+def test_backward_errors():
+    assert call_backward(md=7) == DTYPE
+    assert call_backward(d_out=12) == UNSUP
+    assert call_backward(W=0) == NULLP
+    assert call_backward(step=0) == HYPER
+    assert call_backward(dX=0) == NULLP
+    assert call_backward(dX=DX + 4) == MISAL
+    for name in ("X", "dY", "W", "m", "v"):
+        assert call_backward(dX=BASE[name] + 32) == ALIAS, name
+    assert call_backward(md=I8, dX=BASE["vs"]) == ALIAS
+    # the step's own aliasing rules still apply
+    assert call_backward(m=BASE["X"]) == ALIAS
+
+
+def test_backward_empty_cases():
+    assert call_backward(T=0, d_in=0, dX=0) == OK
+    # T == 0: dX is empty (may be NULL); the zero-gradient step still validates its state
+    assert call_backward(T=0, dX=0, W=0) == NULLP
+
+
+def test_backward_group_errors():
+    assert lib().forge_linear_backward_grouped(None, 1, 64, DX, BF16, 1e-3, 0.9, 0.999, 1e-8, 0.1, 1, None) == NULLP
+    assert call_backward_group([_mat(0)], n=0) == SHAPE
+    assert call_backward_group([_mat(0), _mat(1, d_in=256)]) == SHAPE      # members disagree on d_in
+    assert call_backward_group([_mat(0), _mat(1, d_in=0, d_out=0)]) == SHAPE
+    m0 = _mat(0)
+    assert call_backward_group([m0, _mat(1, X=m0.X)], dX=0) == NULLP
+    assert call_backward_group([m0, _mat(1, X=m0.X)], dX=m0.X) == ALIAS
+    m1 = _mat(1, X=m0.X)
+    assert call_backward_group([m0, m1], dX=m1.dY + 16) == ALIAS
+    assert call_backward_group([m0, m1], md=I8, dX=m1.v_scale) == ALIAS
+
+
+@pytest.mark.skipif(_gpu_visible(), reason="on a GPU machine a valid call would launch on fake pointers")
+def test_backward_valid_arguments_reach_the_device_check():
+    assert call_backward() == NODEV
+    assert call_backward(d_out=0) == NODEV                               # dX zero-filled, no step
+    m0 = _mat(0)
+    assert call_backward_group([m0, _mat(1, X=m0.X, d_out=64), _mat(2, X=m0.X, d_out=0)]) == NODEV
+    assert call_backward_group([_mat(0, d_out=0)]) == NODEV

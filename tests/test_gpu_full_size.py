@@ -111,3 +111,81 @@ def test_maximum_operand_size(T, d_in, d_out, moment):
     if ms is not None:
         gpu.update(m_scale=bits(sel(ms)), v_scale=bits(sel(vs)))
     _say(check_step(gpu, ora, moment, hp=p.hp))
+
+
+# ----------------------------------------------------------------------------- layer-level backward
+
+def _dx_rows_ok(got_rows, dY_rows, Ws, what):
+    """Sampled token rows of dX against the oracle: row t of dX depends only on row t of
+    each dY (and on the whole W), so the oracle on those rows gives the exact values."""
+    from test_gpu_backward import check_dx
+    try:
+        return check_dx(got_rows, list(zip(dY_rows, Ws)))
+    except AssertionError as e:
+        raise AssertionError(f"{what}: {e}") from None
+
+
+def test_backward_one_layer_and_lm_head_sampled_rows():
+    """The backward of lm_head and of the last decoder layer of the sweep at T = 512, in
+    its grouping ([down], [gate, up], [o], [q, k, v]): dX sampled on 8 token rows, the
+    state sampled on 8 rows of each weight."""
+    wl = synth.WORKLOADS["sweep"]
+    step = wl.steps[0]
+    device = torch.device("cuda:0")
+    rng = np.random.default_rng(2607)
+    groups = synth.launch_groups(wl)[:5]             # lm_head, then layer 31's four groups
+    t_rows = _sample(wl.T, rng, 8)
+    tr = torch.from_numpy(t_rows).to(device)
+    for g in groups:
+        tensors, host = [], []
+        for i in g:
+            mat = wl.matrices[i]
+            X, dY = synth.activations(wl.T, mat, wl, step, device=device)
+            W = synth.weight(mat, wl, device=device)
+            m, v = synth.warm_moments(mat, wl, device=device, dtype=torch.bfloat16)
+            rows = torch.from_numpy(_sample(mat.d_out, rng, ROWS_PER_MATRIX)).to(device)
+            p = Problem(bits(X), bits(dY.index_select(1, rows)), bits(W.index_select(0, rows)),
+                        bits(m.index_select(0, rows)), bits(v.index_select(0, rows)), "bf16", hp=dict(wl.hyper))
+            host.append((mat, rows, p, run_oracle(p, step), bits(dY.index_select(0, tr)), bits(W)))
+            tensors.append((X, dY, W, m, v))
+        names = [h[0].name for h in host]
+        _say(f"backward group {names}")
+        dX = torch.empty((wl.T, tensors[0][0].shape[1]), dtype=torch.bfloat16, device=device)
+        forge.forge_linear_backward_grouped(tensors, dX=dX, step=step, **wl.hyper)
+        torch.cuda.synchronize()
+        _say(_dx_rows_ok(bits(dX.index_select(0, tr)), [h[4] for h in host], [h[5] for h in host], names))
+        for (X, dY, W, m, v), (mat, rows, p, ora, _, _) in zip(tensors, host):
+            gpu = dict(W=bits(W.index_select(0, rows)), m=bits(m.index_select(0, rows)),
+                       v=bits(v.index_select(0, rows)))
+            check_step(gpu, ora, "bf16", hp=p.hp)
+
+
+# (T, d_in, d_out): dY (then dX and W) with just under 2^31 elements.  W is zero except on
+# 64 sampled rows, so that dX = dY[:, rows] W[rows, :] exactly and the oracle stays cheap
+# while the kernel still runs its whole K loop.
+DX_MAX_SHAPES = [(33, 8, D_MAX), (33, D_MAX, 8)]
+
+
+@pytest.mark.parametrize("T,d_in,d_out", DX_MAX_SHAPES, ids=["dY-2^31", "dX-2^31"])
+def test_input_grad_maximum_operand_size(T, d_in, d_out):
+    _say(f"input_grad max size T={T} d_in={d_in} d_out={d_out}")
+    device = torch.device("cuda:0")
+    rng = np.random.default_rng(34)
+    dY = synth.gaussian((T, d_out), 1e-3, 7101, device=device)
+    W = synth.gaussian((d_out, d_in), 0.02, 7102, device=device)
+    rows = torch.from_numpy(_sample(d_out, rng, 8)).to(device)
+    if d_out > 64:
+        keep = torch.zeros(d_out, dtype=torch.bool, device=device)
+        keep[rows] = True
+        W[~keep] = 0
+    dX = torch.full((T, d_in), float("nan"), dtype=torch.bfloat16, device=device)
+    forge.forge_input_grad(dY, W, dX)
+    torch.cuda.synchronize()
+    from test_gpu_backward import check_dx
+    if d_in > 64:
+        cols = torch.from_numpy(_sample(d_in, rng, 64)).to(device)
+        got = bits(dX.index_select(1, cols))
+        _say(check_dx(got, [(bits(dY), bits(W.index_select(1, cols)))]))
+        assert not torch.isnan(dX).any()
+    else:
+        _say(check_dx(bits(dX), [(bits(dY.index_select(1, rows)), bits(W.index_select(0, rows)))]))

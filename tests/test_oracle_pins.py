@@ -3,7 +3,8 @@
 Kinds of pin used here (a plausible mistake in the oracle -- a dropped term, a wrong
 sign, a transposed operand, a wrong bias correction -- fails at least one):
 
-* exact rational brute force of G = dY^T X on tiny non-square shapes;
+* exact rational brute force of G = dY^T X and of dX = dY W on tiny non-square shapes;
+* dX is the adjoint of the forward Y = X W^T, and <dX, X> = <G, W> ties it to G;
 * the rank-one closed form of G;
 * Prop. 1 (App. A): summing the oracle's G over any partition of the token axis gives G;
 * closed forms of Algorithm 1's update (step 1 from zero state; zero gradient; beta = 0;
@@ -136,6 +137,86 @@ def test_wgrad_token_partition_invariance(chunk):
 def test_wgrad_empty_token_axis():
     G = oracle.wgrad(np.zeros((0, 8), np.uint16), np.zeros((0, 3), np.uint16))
     assert G.shape == (3, 8) and not G.any()
+
+
+# ------------------------------------------------------------------------- input gradient
+
+def test_input_grad_exact_rationals_nonsquare():
+    T, d_in, d_out = 6, 3, 5
+    dY = bf16_rand((T, d_out), 0.01, 31)
+    W = bf16_rand((d_out, d_in), 0.02, 32)
+    dX = oracle.input_grad(dY, W)
+    assert dX.shape == (T, d_in)
+    Yf, Wf = oracle.bf16_bits_to_f64(dY), oracle.bf16_bits_to_f64(W)
+    for t in range(T):
+        for q in range(d_in):
+            exact = sum(Fraction(Yf[t, p]) * Fraction(Wf[p, q]) for p in range(d_out))
+            bound = d_out * 2.0 ** -53 * sum(abs(Yf[t, p] * Wf[p, q]) for p in range(d_out))
+            assert abs(dX[t, q] - float(exact)) <= bound
+
+
+def test_input_grad_integer_values_exact():
+    rng = np.random.default_rng(3)
+    T, d_in, d_out = 5, 7, 4
+    Yv = rng.integers(-8, 9, (T, d_out))
+    Wv = rng.integers(-8, 9, (d_out, d_in))
+    dX = oracle.input_grad(to_bits(Yv.tolist()), to_bits(Wv.tolist()))
+    assert np.array_equal(dX, (Yv @ Wv).astype(np.float64))
+
+
+def test_input_grad_identity_weight_returns_dy():
+    d = 8
+    dY = bf16_rand((5, d), 1.0, 33)
+    dX = oracle.input_grad(dY, to_bits(np.eye(d).tolist()))
+    assert np.array_equal(dX, oracle.bf16_bits_to_f64(dY))
+
+
+def test_input_grad_is_adjoint_of_forward():
+    """<dX, X> = <dY, Y> for the forward Y = X W^T (Eq. fwd), for any X: the backward is
+    the transpose of the forward map.  Square d_in = d_out with a non-symmetric W, so a
+    transposed weight fails too."""
+    T, d = 9, 12
+    X = oracle.bf16_bits_to_f64(bf16_rand((T, d), 1.0, 34))
+    W = bf16_rand((d, d), 0.02, 35)
+    dY = bf16_rand((T, d), 0.01, 36)
+    Wf, Yf = oracle.bf16_bits_to_f64(W), oracle.bf16_bits_to_f64(dY)
+    assert not np.allclose(Wf, Wf.T)
+    Y = np.array([[sum(X[t, q] * Wf[p, q] for q in range(d)) for p in range(d)] for t in range(T)])
+    lhs = float(np.sum(oracle.input_grad(dY, W) * X))
+    rhs = float(np.sum(Yf * Y))
+    assert abs(lhs - rhs) <= 1e-12 * (np.abs(Yf) @ np.abs(Wf) * np.abs(X)).sum()
+
+
+def test_input_grad_consistent_with_weight_gradient():
+    """<dX, X> = <G, W> with G = dY^T X: both equal sum_{t,p,q} dY[t,p] W[p,q] X[t,q].
+    Ties the input gradient to the separately pinned weight gradient."""
+    T, d_in, d_out = 11, 16, 24
+    X = bf16_rand((T, d_in), 1.0, 37)
+    dY = bf16_rand((T, d_out), 0.01, 38)
+    W = bf16_rand((d_out, d_in), 0.02, 39)
+    Xf, Wf = oracle.bf16_bits_to_f64(X), oracle.bf16_bits_to_f64(W)
+    a = float(np.sum(oracle.input_grad(dY, W) * Xf))
+    b = float(np.sum(oracle.wgrad(X, dY) * Wf))
+    scale = float((np.abs(oracle.bf16_bits_to_f64(dY)) @ np.abs(Wf) * np.abs(Xf)).sum())
+    assert abs(a - b) <= 1e-12 * scale
+
+
+def test_input_grad_empty_axes():
+    assert not oracle.input_grad(np.zeros((4, 0), np.uint16), np.zeros((0, 8), np.uint16)).any()
+    assert oracle.input_grad(np.zeros((4, 0), np.uint16), np.zeros((0, 8), np.uint16)).shape == (4, 8)
+    assert oracle.input_grad(np.zeros((0, 8), np.uint16), np.zeros((8, 16), np.uint16)).shape == (0, 16)
+
+
+def test_linear_backward_reads_pre_update_weight():
+    """The ordering remark of App. A: dX comes from W before the step, not after it."""
+    T, d_in, d_out = 16, 24, 8
+    X = bf16_rand((T, d_in), 1.0, 40)
+    dY = bf16_rand((T, d_out), 0.01, 41)
+    W = bf16_rand((d_out, d_in), 0.02, 42)
+    z = np.zeros((d_out, d_in), np.float32)
+    out = oracle.linear_backward(X, dY, W, z, z, moment_dtype=MOMENT_F32, step=1, **HP)
+    assert np.array_equal(out["dX"], oracle.input_grad(dY, W))
+    assert not np.array_equal(out["dX"], oracle.input_grad(dY, out["W"]))
 
 
 # ------------------------------------------------------------------------- AdamW update
