@@ -317,13 +317,16 @@ def main():
 def micro(device, reps, warmup, d=4096, token_counts=(512, 4096)):
     """Update-path microbenchmark (App. D): on the q/o_proj shape d x d, the average
     duration of the store-G control (the same tile kernel with an epilogue that stores G
-    as bf16 instead of updating the optimizer state) and of the fused AdamW step (bf16 and
-    fp32 moments); the marginal cost of the update is their difference.  Also the
-    layer-level backward: dX = dY W alone and followed by the fused step.  Each figure is
+    as bf16 instead of updating the optimizer state) and of the fused step with every
+    update rule (AdamW and the other families, fp32 and bf16 state); the marginal cost of
+    an update is the difference.  Also the layer-level backward: dX = dY W alone and
+    followed by the fused step.  Each figure is
     `reps` back-to-back launches between two events on the launch stream, after `warmup`."""
     import torch
     from paper_2606_22932_amd import forge, synth
     hp = dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.1)
+    rule_hp = {n: dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.01) for n in forge.OPTIMIZERS}
+    rule_hp["muon_accumulate"] = dict(lr=0.0, beta1=0.95)
     stream = torch.cuda.current_stream()
 
     def avg_us(fn):
@@ -358,6 +361,18 @@ def micro(device, reps, warmup, d=4096, token_counts=(512, 4096)):
                                                                            **hp))
         r["marginal_adamw_bf16_us"] = r["adamw_bf16_us"] - r["store_g_control_us"]
         r["marginal_adamw_f32_us"] = r["adamw_f32_us"] - r["store_g_control_us"]
+        # every update rule, by state count, on fp32 and bf16 state (the family table's rules)
+        fam = {}
+        for name in ("sgd", "sgd_momentum", "adagrad", "rmsprop", "lion", "muon_accumulate", "adamax", "adamw",
+                     "nadam", "radam"):
+            ns = forge.OPTIMIZER_STATES[name]
+            for tag, (s1, s2) in (("f32", (mf, vf)), ("bf16", (mb, vb))):
+                Wr = None if name == "muon_accumulate" else W
+                us = avg_us(lambda: forge.forge_linear_step_opt(X, dY, Wr, s1, s2, optimizer=name, step=100,
+                                                                **rule_hp[name]))
+                fam[f"{name}_{tag}"] = {"states": ns, "us": round(us, 2),
+                                        "marginal_us": round(us - r["store_g_control_us"], 2)}
+        r["rules"] = fam
         rows.append({k: (round(v, 2) if isinstance(v, float) else v) for k, v in r.items()})
         log(f"micro: {rows[-1]}")
         del X, dY, W, G, dX, mb, vb, mf, vf

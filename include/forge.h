@@ -75,7 +75,8 @@ typedef enum {
     FORGE_ERR_MISALIGNED = 6,        /* a tensor pointer not 16-byte aligned */
     FORGE_ERR_ALIASING = 7,          /* an output overlaps another tensor */
     FORGE_ERR_NO_DEVICE = 8,         /* no usable gfx950 device is current */
-    FORGE_ERR_LAUNCH = 9             /* the kernel launch failed (hipGetLastError) */
+    FORGE_ERR_LAUNCH = 9,            /* the kernel launch failed (hipGetLastError) */
+    FORGE_ERR_INVALID_OPTIMIZER = 10 /* unknown optimizer code */
 } forge_status;
 
 /*
@@ -137,6 +138,85 @@ typedef struct forge_matrix {
 FORGE_API forge_status forge_linear_step_grouped(const forge_matrix *mats, int32_t n, int64_t T,
                                        int32_t moment_dtype, float lr, float beta1, float beta2,
                                        float eps, float weight_decay, int64_t step, void *stream);
+
+/*
+ * Update rules of forge_linear_step_opt: the coordinate-wise optimizer families whose state
+ * update reads only the gradient's own coordinate, so that they fuse into the tile epilogue
+ * like AdamW (App. A, Def. 1; the family table of App. I), and Muon's momentum accumulate.
+ * The paper does not restate these rules; each follows the reference implementation it was
+ * checked against there (PyTorch's torch.optim for all but Lion, whose rule is that of its
+ * authors).  G is the weight gradient, t the step, "gg" the gradient with coupled weight
+ * decay added, gg = G + wd W; s1 and s2 are the state tensors.
+ *
+ *   FORGE_OPT_ADAMW          s1 = m, s2 = v: exactly forge_linear_step (decoupled decay)
+ *   FORGE_OPT_SGD            no state: W -= lr gg
+ *   FORGE_OPT_SGD_MOMENTUM   s1 = b: b = beta1 b + gg; W -= lr b       (beta1 = momentum)
+ *   FORGE_OPT_ADAGRAD        s1 = sum: sum += gg^2; W -= clr gg / (sqrt(sum) + eps),
+ *                            clr = lr / (1 + (t - 1) lr_decay)
+ *   FORGE_OPT_RMSPROP        s1 = a: a = beta2 a + (1 - beta2) gg^2; W -= lr gg / (sqrt(a) + eps)
+ *                            (beta2 = alpha)
+ *   FORGE_OPT_LION           s1 = m: W = (1 - lr wd) W - lr sign(beta1 m + (1 - beta1) G);
+ *                            m = beta2 m + (1 - beta2) G
+ *   FORGE_OPT_NADAM          s1 = m, s2 = v (Adam moments of gg); with mu_i =
+ *                            beta1 (1 - 0.5 * 0.96^(i momentum_decay)) and P_t = mu_1 ... mu_t:
+ *                            W -= lr [(1 - mu_t)/(1 - P_t) gg + mu_{t+1}/(1 - P_t mu_{t+1}) m]
+ *                                 / (sqrt(v / (1 - beta2^t)) + eps)
+ *   FORGE_OPT_RADAM          s1 = m, s2 = v (Adam moments of gg); rho_inf = 2/(1 - beta2) - 1,
+ *                            rho_t = rho_inf - 2 t beta2^t / (1 - beta2^t); if rho_t > 5:
+ *                            W -= lr r (m / (1 - beta1^t)) sqrt(1 - beta2^t) / (sqrt(v) + eps),
+ *                            r = sqrt((rho_t-4)(rho_t-2) rho_inf / ((rho_inf-4)(rho_inf-2) rho_t));
+ *                            else W -= lr m / (1 - beta1^t)
+ *   FORGE_OPT_ADAMAX         s1 = m, s2 = u: m = beta1 m + (1 - beta1) gg;
+ *                            u = max(beta2 u, |gg| + eps); W -= lr / (1 - beta1^t) m / u
+ *   FORGE_OPT_MUON_ACCUMULATE  s1 = B: B = beta1 B + G (the GEMM's beta; regime 2 of App. A).
+ *                            W is neither read nor written (the orthogonalising weight update
+ *                            reads B only and runs outside this call).  Over micro-batches of
+ *                            one step pass beta1 = mu on the first and 1 on the others.
+ */
+typedef enum {
+    FORGE_OPT_ADAMW = 0,
+    FORGE_OPT_SGD = 1,
+    FORGE_OPT_SGD_MOMENTUM = 2,
+    FORGE_OPT_ADAGRAD = 3,
+    FORGE_OPT_RMSPROP = 4,
+    FORGE_OPT_LION = 5,
+    FORGE_OPT_NADAM = 6,
+    FORGE_OPT_RADAM = 7,
+    FORGE_OPT_ADAMAX = 8,
+    FORGE_OPT_MUON_ACCUMULATE = 9
+} forge_optimizer;
+
+/* Hyper-parameters of forge_linear_step_opt; a rule reads only the fields it names above. */
+typedef struct forge_hparams {
+    float lr;              /* >= 0 */
+    float beta1;           /* [0, 1); Muon accumulate: [0, 1] */
+    float beta2;           /* [0, 1) */
+    float eps;             /* > 0 where used */
+    float weight_decay;    /* finite */
+    float lr_decay;        /* Adagrad: >= 0 */
+    float momentum_decay;  /* NAdam: >= 0 (PyTorch's default is 0.004) */
+} forge_hparams;
+
+/*
+ * forge_linear_step_opt -- the fused step with update rule `optimizer` on fp32 or bf16 state.
+ *
+ *   X, dY, T, d_in, d_out, step, stream   as in forge_linear_step
+ *   W        bf16 [d_out, d_in], in/out (unused, may be NULL, for FORGE_OPT_MUON_ACCUMULATE)
+ *   s1, s2   [d_out, d_in] state tensors in `state_dtype` (FORGE_MOMENT_F32 or _BF16), in/out;
+ *            a rule with fewer states ignores the others (they may be NULL)
+ *   hp       host pointer, read during the call only
+ *
+ * The tile mainloop is the one of forge_linear_step; only the epilogue differs, and W, the
+ * states and the output roundings (bf16 / fp32, round-to-nearest-even) are handled as there.
+ * Errors: FORGE_ERR_INVALID_OPTIMIZER for an unknown code; FORGE_ERR_INVALID_DTYPE for a
+ * state dtype other than fp32 / bf16 (int8 moments: forge_linear_step); NULL hp:
+ * FORGE_ERR_NULL_POINTER; out-of-range fields the rule reads: FORGE_ERR_INVALID_HYPERPARAM;
+ * the other checks as in forge_linear_step.
+ */
+FORGE_API forge_status forge_linear_step_opt(const void *X, const void *dY, void *W, void *s1, void *s2,
+                                             int64_t T, int64_t d_in, int64_t d_out, int32_t optimizer,
+                                             int32_t state_dtype, const forge_hparams *hp, int64_t step,
+                                             void *stream);
 
 /*
  * forge_input_grad -- the layer's input gradient dX = dY W (Algorithm 1, first line; the

@@ -22,6 +22,12 @@ _SRC = os.path.join(_HERE, "forge_oracle.c")
 _LIB = os.path.join(_HERE, "libforge_oracle.so")
 
 MOMENT_F32, MOMENT_BF16, MOMENT_I8 = 0, 1, 2
+# Update rules (forge_oracle_rule_step); AdamW is ``adamw``.
+OPT_ADAMW, OPT_SGD, OPT_SGD_MOMENTUM, OPT_ADAGRAD, OPT_RMSPROP, OPT_LION = 0, 1, 2, 3, 4, 5
+OPT_NADAM, OPT_RADAM, OPT_ADAMAX, OPT_MUON = 6, 7, 8, 9
+# state tensors of each rule, and whether it updates W
+RULE_STATES = {OPT_ADAMW: 2, OPT_SGD: 0, OPT_SGD_MOMENTUM: 1, OPT_ADAGRAD: 1, OPT_RMSPROP: 1, OPT_LION: 1,
+               OPT_NADAM: 2, OPT_RADAM: 2, OPT_ADAMAX: 2, OPT_MUON: 1}
 I8_BLOCK = 256
 
 _lock = threading.Lock()
@@ -62,6 +68,9 @@ def _load():
             lib.forge_oracle_adamw.argtypes = [P, P, P, P, P, P, I64, I64, I32, F32, F32, F32, F32,
                                                F32, I64, I32, P, P, P, P, P]
             lib.forge_oracle_adamw.restype = None
+            lib.forge_oracle_rule_step.argtypes = [P, P, P, P, I64, I64, I32, I32, F32, F32, F32, F32, F32,
+                                                   F32, F32, I64, P, P, P, P]
+            lib.forge_oracle_rule_step.restype = None
             lib.forge_oracle_num_threads.argtypes = []
             lib.forge_oracle_num_threads.restype = I32
             _lib = lib
@@ -182,6 +191,31 @@ def adamw(G, W, m, v, *, moment_dtype, lr, beta1, beta2, eps, weight_decay, step
     if qm is not None:
         out.update(qm=qm, qv=qv)
     return out
+
+
+def rule_step(G, W, s1=None, s2=None, *, opt, state_dtype, lr, beta1=0.0, beta2=0.0, eps=1e-8,
+              weight_decay=0.0, lr_decay=0.0, momentum_decay=0.004, step):
+    """One step of update rule ``opt`` (not AdamW) on an fp64 gradient; inputs are not modified.
+
+    W: bf16 bits [d_out, d_in]; s1, s2: float32 or bf16-bits state per ``state_dtype`` (None
+    for states the rule does not have).  Returns W, s1, s2 rounded to storage, their fp64
+    values W64, s1_64, s2_64, and ``aux`` (Lion: the argument of the sign).
+    """
+    if opt == OPT_ADAMW:
+        raise ValueError("AdamW: use adamw()")
+    G = _c(G, np.float64)
+    d_out, d_in = G.shape
+    W = _c(W, np.uint16).copy()
+    sdt = np.float32 if state_dtype == MOMENT_F32 else np.uint16
+    ns = RULE_STATES[opt]
+    s1 = _c(s1, sdt).copy() if ns >= 1 else None
+    s2 = _c(s2, sdt).copy() if ns >= 2 else None
+    W64, S1, S2, AUX = (np.zeros((d_out, d_in), np.float64) for _ in range(4))
+    _load().forge_oracle_rule_step(
+        _ptr(G), _ptr(W), _ptr(s1), _ptr(s2), d_in, d_out, int(opt), int(state_dtype), float(lr),
+        float(beta1), float(beta2), float(eps), float(weight_decay), float(lr_decay), float(momentum_decay),
+        int(step), _ptr(W64), _ptr(S1), _ptr(S2), _ptr(AUX))
+    return dict(W=W, s1=s1, s2=s2, W64=W64, s1_64=S1, s2_64=S2, aux=AUX)
 
 
 def linear_step(X, dY, W, m, v, **kw):

@@ -29,6 +29,14 @@
  * Hyper-parameters arrive as the fp32 values the GPU receives; they are promoted
  * to fp64 here, so lr = 1e-3 means (double)(float)1e-3.
  *
+ * Other update rules (forge_oracle_rule_step): the coordinate-wise optimizer families of
+ * the paper's family table (App. I) and Muon's momentum accumulate (regime 2 of App. A).
+ * The paper states that each was checked against its reference implementation and does
+ * not restate the rules, so each is written here from that implementation's published
+ * algorithm (torch.optim's documentation for SGD, Adagrad, RMSprop, NAdam, RAdam, Adamax;
+ * the Lion paper's algorithm for Lion), in fp64, coupled weight decay (gg = g + wd w)
+ * where those algorithms use it, decoupled for Lion.
+ *
  * The layer-level backward adds one more quantity, computed before the update:
  *   0. the input gradient dX = dY W from the pre-update weight (Algorithm 1, first
  *      line; the ordering remark of App. A), dX[t][q] = sum_p dY[t][p] * W[p][q],
@@ -322,6 +330,150 @@ void forge_oracle_linear_step(const uint16_t *X, const uint16_t *dY, uint16_t *W
     forge_oracle_adamw(G, W, m, v, m_scale, v_scale, d_in, d_out, moment_dtype, lr, beta1,
                        beta2, eps, weight_decay, step, round_grad_to_bf16, W64, m64, v64, qm, qv);
     if (!G_out) free(G);
+}
+
+/* ------------------------------------------------------------- other update rules */
+
+enum {
+    ORACLE_OPT_ADAMW = 0, ORACLE_OPT_SGD = 1, ORACLE_OPT_SGD_MOMENTUM = 2, ORACLE_OPT_ADAGRAD = 3,
+    ORACLE_OPT_RMSPROP = 4, ORACLE_OPT_LION = 5, ORACLE_OPT_NADAM = 6, ORACLE_OPT_RADAM = 7,
+    ORACLE_OPT_ADAMAX = 8, ORACLE_OPT_MUON = 9
+};
+
+static double load_state(const void *s, int64_t k, int dtype)
+{
+    if (!s) return 0.0;
+    if (dtype == ORACLE_MOMENT_F32) return (double)((const float *)s)[k];
+    return forge_oracle_bf16_to_f64(((const uint16_t *)s)[k]);
+}
+
+static void store_state(void *s, int64_t k, int dtype, double x)
+{
+    if (!s) return;
+    if (dtype == ORACLE_MOMENT_F32) ((float *)s)[k] = (float)x;   /* C cast: round to nearest even */
+    else ((uint16_t *)s)[k] = forge_oracle_f64_to_bf16(x);
+}
+
+/*
+ * One step of update rule `opt` on the fp64 gradient G [d_out, d_in] (AdamW has its own
+ * routine above).  W: bf16 bits [d_out, d_in], in/out (untouched by the Muon accumulate).
+ * s1, s2: state tensors in `state_dtype` (fp32 or bf16), in/out; NULL for a state the rule
+ * does not have.  W64, S1, S2 (optional): the unrounded fp64 results.  AUX (optional): the
+ * argument of Lion's sign, which a test needs to recognise elements where the sign is
+ * decided within rounding error.  Hyper-parameters are promoted from fp32 to fp64.
+ *
+ *   SGD       gg = g + wd w;  w' = w - lr gg
+ *   SGD-m     b' = beta1 b + gg;  w' = w - lr b'            (dampening 0, no Nesterov)
+ *   Adagrad   s' = s + gg^2;  w' = w - clr gg / (sqrt(s') + eps),  clr = lr / (1 + (t-1) lr_decay)
+ *   RMSprop   a' = beta2 a + (1 - beta2) gg^2;  w' = w - lr gg / (sqrt(a') + eps)
+ *   Lion      c = beta1 m + (1 - beta1) g;  w' = w (1 - lr wd) - lr sign(c);
+ *             m' = beta2 m + (1 - beta2) g
+ *   NAdam     mu_i = beta1 (1 - 0.5 * 0.96^(i psi)), P_t = prod_{i<=t} mu_i;
+ *             m', v' the Adam moments of gg;  d = sqrt(v' / (1 - beta2^t)) + eps;
+ *             w' = w - lr (1 - mu_t) / (1 - P_t) gg / d - lr mu_{t+1} / (1 - P_t mu_{t+1}) m' / d
+ *   RAdam     m', v' the Adam moments of gg;  mhat = m' / (1 - beta1^t);
+ *             rho_inf = 2 / (1 - beta2) - 1;  rho_t = rho_inf - 2 t beta2^t / (1 - beta2^t);
+ *             rho_t > 5: w' = w - lr mhat r sqrt(1 - beta2^t) / (sqrt(v') + eps),
+ *                        r = sqrt((rho_t - 4)(rho_t - 2) rho_inf / ((rho_inf - 4)(rho_inf - 2) rho_t));
+ *             else       w' = w - lr mhat
+ *   Adamax    m' = beta1 m + (1 - beta1) gg;  u' = max(beta2 u, |gg| + eps);
+ *             w' = w - lr / (1 - beta1^t) m' / u'
+ *   Muon      B' = beta1 B + g  (W unchanged)
+ */
+void forge_oracle_rule_step(const double *G, uint16_t *W, void *s1, void *s2, int64_t d_in, int64_t d_out,
+                            int opt, int state_dtype, float lr, float beta1, float beta2, float eps,
+                            float weight_decay, float lr_decay, float momentum_decay, int64_t step,
+                            double *W64, double *S1, double *S2, double *AUX)
+{
+    const double eta = lr, b1 = beta1, b2 = beta2, ep = eps, lam = weight_decay, t = (double)step;
+    const double bc1 = 1.0 - pow(b1, t), bc2 = 1.0 - pow(b2, t);
+    /* NAdam's momentum schedule */
+    double mu_t = 0.0, mu_next = 0.0, prod = 1.0;
+    if (opt == ORACLE_OPT_NADAM) {
+        for (int64_t i = 1; i <= step; ++i)
+            prod *= b1 * (1.0 - 0.5 * pow(0.96, (double)i * (double)momentum_decay));
+        mu_t = b1 * (1.0 - 0.5 * pow(0.96, t * (double)momentum_decay));
+        mu_next = b1 * (1.0 - 0.5 * pow(0.96, (t + 1.0) * (double)momentum_decay));
+    }
+    /* RAdam's rectification */
+    double rho_inf = 0.0, rho_t = 0.0, rect = 0.0;
+    if (opt == ORACLE_OPT_RADAM) {
+        rho_inf = 2.0 / (1.0 - b2) - 1.0;
+        rho_t = rho_inf - 2.0 * t * pow(b2, t) / bc2;
+        if (rho_t > 5.0)
+            rect = sqrt((rho_t - 4.0) * (rho_t - 2.0) * rho_inf / ((rho_inf - 4.0) * (rho_inf - 2.0) * rho_t));
+    }
+    const double clr = eta / (1.0 + (t - 1.0) * (double)lr_decay);
+
+#pragma omp parallel for schedule(static)
+    for (int64_t k = 0; k < d_in * d_out; ++k) {
+        const double g = G[k];
+        const double w = forge_oracle_bf16_to_f64(W[k]);
+        const double a = load_state(s1, k, state_dtype);
+        const double b = load_state(s2, k, state_dtype);
+        const double gg = g + lam * w;
+        double w1 = w, a1 = a, bb1 = b, aux = 0.0;
+        switch (opt) {
+        case ORACLE_OPT_SGD:
+            w1 = w - eta * gg;
+            break;
+        case ORACLE_OPT_SGD_MOMENTUM:
+            a1 = b1 * a + gg;
+            w1 = w - eta * a1;
+            break;
+        case ORACLE_OPT_ADAGRAD:
+            a1 = a + gg * gg;
+            w1 = w - clr * gg / (sqrt(a1) + ep);
+            break;
+        case ORACLE_OPT_RMSPROP:
+            a1 = b2 * a + (1.0 - b2) * gg * gg;
+            w1 = w - eta * gg / (sqrt(a1) + ep);
+            break;
+        case ORACLE_OPT_LION: {
+            const double c = b1 * a + (1.0 - b1) * g;
+            const double sg = c > 0.0 ? 1.0 : (c < 0.0 ? -1.0 : 0.0);
+            aux = c;
+            w1 = w * (1.0 - eta * lam) - eta * sg;
+            a1 = b2 * a + (1.0 - b2) * g;
+            break;
+        }
+        case ORACLE_OPT_NADAM: {
+            a1 = b1 * a + (1.0 - b1) * gg;
+            bb1 = b2 * b + (1.0 - b2) * gg * gg;
+            const double d = sqrt(bb1 / bc2) + ep;
+            w1 = w - eta * (1.0 - mu_t) / (1.0 - prod) * gg / d - eta * mu_next / (1.0 - prod * mu_next) * a1 / d;
+            break;
+        }
+        case ORACLE_OPT_RADAM: {
+            a1 = b1 * a + (1.0 - b1) * gg;
+            bb1 = b2 * b + (1.0 - b2) * gg * gg;
+            const double mhat = a1 / bc1;
+            if (rho_t > 5.0) w1 = w - eta * mhat * rect * sqrt(bc2) / (sqrt(bb1) + ep);
+            else w1 = w - eta * mhat;
+            break;
+        }
+        case ORACLE_OPT_ADAMAX: {
+            a1 = b1 * a + (1.0 - b1) * gg;
+            const double n = fabs(gg) + ep;
+            bb1 = b2 * b > n ? b2 * b : n;
+            w1 = w - eta / bc1 * a1 / bb1;
+            break;
+        }
+        case ORACLE_OPT_MUON:
+            a1 = b1 * a + g;
+            w1 = w;
+            break;
+        default:
+            break;
+        }
+        if (opt != ORACLE_OPT_MUON) W[k] = forge_oracle_f64_to_bf16(w1);
+        store_state(s1, k, state_dtype, a1);
+        store_state(s2, k, state_dtype, bb1);
+        if (W64) W64[k] = w1;
+        if (S1) S1[k] = a1;
+        if (S2) S2[k] = bb1;
+        if (AUX) AUX[k] = aux;
+    }
 }
 
 int forge_oracle_num_threads(void)

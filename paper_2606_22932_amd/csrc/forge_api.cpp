@@ -231,6 +231,110 @@ forge_status plan_group(const forge_matrix *mats, int32_t n, int64_t T, int32_t 
     return FORGE_OK;
 }
 
+// ----------------------------------------------------------------- update rules
+
+struct RuleInfo {
+    int epi;        // forge_impl::EpiKind
+    int nstate;     // state tensors read and written
+    bool uses_w;    // reads and writes W
+};
+
+bool rule_info(int32_t opt, RuleInfo &r)
+{
+    using namespace forge_impl;
+    switch (opt) {
+    case FORGE_OPT_ADAMW: r = {EPI_ADAMW, 2, true}; return true;
+    case FORGE_OPT_SGD: r = {EPI_SGD, 0, true}; return true;
+    case FORGE_OPT_SGD_MOMENTUM: r = {EPI_SGDM, 1, true}; return true;
+    case FORGE_OPT_ADAGRAD: r = {EPI_ADAGRAD, 1, true}; return true;
+    case FORGE_OPT_RMSPROP: r = {EPI_RMSPROP, 1, true}; return true;
+    case FORGE_OPT_LION: r = {EPI_LION, 1, true}; return true;
+    case FORGE_OPT_NADAM: r = {EPI_NADAM, 2, true}; return true;
+    case FORGE_OPT_RADAM: r = {EPI_RADAM, 2, true}; return true;
+    case FORGE_OPT_ADAMAX: r = {EPI_ADAMAX, 2, true}; return true;
+    case FORGE_OPT_MUON_ACCUMULATE: r = {EPI_MUON, 1, false}; return true;
+    default: return false;
+    }
+}
+
+bool unit_open(float b) { return finite(b) && b >= 0.0f && b < 1.0f; }
+
+// The fields each rule reads must be in range (see forge.h).
+forge_status check_rule_hyper(int32_t opt, const forge_hparams &p, int64_t step)
+{
+    if (step < 1) return FORGE_ERR_INVALID_HYPERPARAM;
+    if (!finite(p.lr) || !(p.lr >= 0.0f) || !finite(p.weight_decay)) return FORGE_ERR_INVALID_HYPERPARAM;
+    const bool eps_ok = finite(p.eps) && p.eps > 0.0f;
+    bool ok = true;
+    switch (opt) {
+    case FORGE_OPT_ADAMW:
+    case FORGE_OPT_RADAM:
+    case FORGE_OPT_ADAMAX: ok = unit_open(p.beta1) && unit_open(p.beta2) && eps_ok; break;
+    case FORGE_OPT_NADAM:
+        ok = unit_open(p.beta1) && unit_open(p.beta2) && eps_ok && finite(p.momentum_decay) &&
+             p.momentum_decay >= 0.0f;
+        break;
+    case FORGE_OPT_SGD: break;
+    case FORGE_OPT_SGD_MOMENTUM: ok = unit_open(p.beta1); break;
+    case FORGE_OPT_ADAGRAD: ok = eps_ok && finite(p.lr_decay) && p.lr_decay >= 0.0f; break;
+    case FORGE_OPT_RMSPROP: ok = unit_open(p.beta2) && eps_ok; break;
+    case FORGE_OPT_LION: ok = unit_open(p.beta1) && unit_open(p.beta2); break;
+    case FORGE_OPT_MUON_ACCUMULATE: ok = finite(p.beta1) && p.beta1 >= 0.0f && p.beta1 <= 1.0f; break;
+    default: ok = false;
+    }
+    return ok ? FORGE_OK : FORGE_ERR_INVALID_HYPERPARAM;
+}
+
+// Per-call scalars of a rule, in fp64, rounded once to fp32 (the formulas of forge.h).
+Hyper make_rule_hyper(int32_t opt, const forge_hparams &p, int64_t step)
+{
+    if (opt == FORGE_OPT_ADAMW) return make_hyper(p.lr, p.beta1, p.beta2, p.eps, p.weight_decay, step);
+    const double t = static_cast<double>(step);
+    const double lr = p.lr, b1 = p.beta1, b2 = p.beta2, wd = p.weight_decay;
+    const double bc1 = 1.0 - std::pow(b1, t), bc2 = 1.0 - std::pow(b2, t);
+    Hyper h;
+    std::memset(&h, 0, sizeof h);
+    h.b1 = p.beta1;
+    h.c1 = static_cast<float>(1.0 - b1);
+    h.b2 = p.beta2;
+    h.c2 = static_cast<float>(1.0 - b2);
+    h.eps = p.eps;
+    h.lr = p.lr;
+    h.wd = p.weight_decay;
+    h.wdf = static_cast<float>(1.0 - lr * wd);
+    switch (opt) {
+    case FORGE_OPT_ADAGRAD: h.lr = static_cast<float>(lr / (1.0 + (t - 1.0) * p.lr_decay)); break;
+    case FORGE_OPT_NADAM: {
+        const double psi = p.momentum_decay;
+        auto mu = [&](double i) { return b1 * (1.0 - 0.5 * std::pow(0.96, i * psi)); };
+        double prod = 1.0;
+        for (int64_t i = 1; i <= step; ++i) prod *= mu(static_cast<double>(i));
+        const double mu_t = mu(t), mu_n = mu(t + 1.0);
+        h.inv_sqrt_bc2 = static_cast<float>(1.0 / std::sqrt(bc2));
+        h.ka = static_cast<float>(lr * (1.0 - mu_t) / (1.0 - prod));
+        h.kb = static_cast<float>(lr * mu_n / (1.0 - prod * mu_n));
+        break;
+    }
+    case FORGE_OPT_RADAM: {
+        const double rho_inf = 2.0 / (1.0 - b2) - 1.0;
+        const double rho_t = rho_inf - 2.0 * t * std::pow(b2, t) / bc2;
+        if (rho_t > 5.0) {
+            const double r = std::sqrt((rho_t - 4.0) * (rho_t - 2.0) * rho_inf /
+                                       ((rho_inf - 4.0) * (rho_inf - 2.0) * rho_t));
+            h.ka = static_cast<float>(lr * r * std::sqrt(bc2) / bc1);
+            h.kb = 0.0f;
+        } else {
+            h.ka = 0.0f;
+            h.kb = static_cast<float>(lr / bc1);
+        }
+        break;
+    }
+    case FORGE_OPT_ADAMAX: h.lr_bc1 = static_cast<float>(lr / bc1); break;
+    default: break;
+    }
+    return h;
+}
+
 }  // namespace
 
 extern "C" {
@@ -250,6 +354,7 @@ const char *forge_status_string(int32_t s)
     case FORGE_ERR_ALIASING: return "FORGE_ERR_ALIASING: an output tensor overlaps another tensor";
     case FORGE_ERR_NO_DEVICE: return "FORGE_ERR_NO_DEVICE: no gfx950 device is current";
     case FORGE_ERR_LAUNCH: return "FORGE_ERR_LAUNCH: kernel launch failed";
+    case FORGE_ERR_INVALID_OPTIMIZER: return "FORGE_ERR_INVALID_OPTIMIZER: unknown optimizer code";
     default: return "unknown forge_status";
     }
 }
@@ -382,6 +487,46 @@ forge_status forge_linear_backward(const void *X, const void *dY, void *W, void 
     const forge_matrix x{X, dY, W, m, v, m_scale, v_scale, d_in, d_out};
     return forge_linear_backward_grouped(&x, 1, T, dX, md, lr, beta1, beta2, eps, weight_decay, step,
                                          stream);
+}
+
+forge_status forge_linear_step_opt(const void *X, const void *dY, void *W, void *s1, void *s2, int64_t T,
+                                   int64_t d_in, int64_t d_out, int32_t opt, int32_t md,
+                                   const forge_hparams *hp, int64_t step, void *stream)
+{
+    forge_status s;
+    bool empty = false;
+    RuleInfo r;
+    if (!rule_info(opt, r)) return FORGE_ERR_INVALID_OPTIMIZER;
+    if (md != FORGE_MOMENT_F32 && md != FORGE_MOMENT_BF16) return FORGE_ERR_INVALID_DTYPE;
+    if (!hp) return FORGE_ERR_NULL_POINTER;
+    if ((s = check_shape(T, d_in, d_out, empty)) != FORGE_OK) return s;
+    if (empty) return FORGE_OK;
+    if ((s = check_inputs(X, dY, T, d_in, d_out)) != FORGE_OK) return s;
+    void *t[3] = {r.uses_w ? W : nullptr, r.nstate >= 1 ? s1 : nullptr, r.nstate >= 2 ? s2 : nullptr};
+    const bool need[3] = {r.uses_w, r.nstate >= 1, r.nstate >= 2};
+    const int64_t P = d_in * d_out;
+    const int64_t bytes[3] = {2 * P, moment_bytes(md) * P, moment_bytes(md) * P};
+    StateSet st;
+    for (int k = 0; k < 3; ++k) {
+        if (!need[k]) continue;
+        if (!t[k]) return FORGE_ERR_NULL_POINTER;
+        if (!aligned16(t[k])) return FORGE_ERR_MISALIGNED;
+        st.r[st.n++] = range_of(t[k], bytes[k]);
+    }
+    for (int i = 0; i < st.n; ++i)
+        for (int j = i + 1; j < st.n; ++j)
+            if (overlap(st.r[i], st.r[j])) return FORGE_ERR_ALIASING;
+    if ((s = check_rule_hyper(opt, *hp, step)) != FORGE_OK) return s;
+    if (T > 0 && (!disjoint_from(st, range_of(X, 2 * T * d_in)) || !disjoint_from(st, range_of(dY, 2 * T * d_out))))
+        return FORGE_ERR_ALIASING;
+    if ((s = check_device()) != FORGE_OK) return s;
+
+    Args a = base_args(X, dY, T, d_in, d_out);
+    a.W = static_cast<uint16_t *>(t[0]);
+    a.m = t[1];
+    a.v = t[2];
+    a.h = make_rule_hyper(opt, *hp, step);
+    return from_hip(forge_impl::launch_fused_rule(&a, 1, r.epi, md, static_cast<hipStream_t>(stream)));
 }
 
 forge_status forge_wgrad(const void *X, const void *dY, void *G, int64_t T, int64_t d_in,

@@ -7,15 +7,20 @@
 
 namespace forge_impl {
 
-// Scalars of one AdamW step, precomputed on the host in fp64 and rounded to fp32
-// (Algorithm 1: the state recurrences and the bias-corrected, decoupled update).
+// Scalars of one optimizer step, precomputed on the host in fp64 and rounded to fp32.  For
+// AdamW (Algorithm 1: the state recurrences and the bias-corrected, decoupled update) the
+// first eight are used; the other rules of the family table read the fields named in their
+// element functions (forge_kernels.hip).
 struct Hyper {
-    float b1, c1;          // beta1, 1 - beta1
+    float b1, c1;          // beta1, 1 - beta1 (AdamW); the first decay of the other rules
     float b2, c2;          // beta2, 1 - beta2
     float lr_bc1;          // lr / (1 - beta1^t)
     float inv_sqrt_bc2;    // 1 / sqrt(1 - beta2^t)
     float eps;
-    float wdf;             // 1 - lr * weight_decay
+    float wdf;             // 1 - lr * weight_decay (decoupled decay)
+    float lr;              // learning rate (Adagrad: lr / (1 + (t-1) lr_decay))
+    float wd;              // weight decay added to the gradient (coupled decay)
+    float ka, kb;          // NAdam, RAdam: step coefficients of their two update terms
 };
 
 // Everything a launch needs; passed by value as the kernel argument.
@@ -63,7 +68,14 @@ struct DxArgs {
 };
 
 enum MomentKind { MK_F32 = 0, MK_BF16 = 1, MK_I8 = 2 };
-enum EpiKind { EPI_ADAMW = 0, EPI_STORE_BF16 = 1, EPI_STORE_F32 = 2 };
+// Tile epilogues of the fused kernel: the update rules (each a per-element function of G,
+// W and the rule's state), and the store-G control.
+enum EpiKind {
+    EPI_ADAMW = 0, EPI_STORE_BF16 = 1, EPI_STORE_F32 = 2,
+    EPI_SGD = 3, EPI_SGDM = 4, EPI_ADAGRAD = 5, EPI_RMSPROP = 6, EPI_LION = 7,
+    EPI_NADAM = 8, EPI_RADAM = 9, EPI_ADAMAX = 10, EPI_MUON = 11,
+    EPI_COUNT = 12
+};
 
 struct TileShape { int rows, cols, tokens; };
 
@@ -74,6 +86,9 @@ TileShape tile_shape(int moment_kind);
 hipError_t launch_fused(const Args &a, int moment_kind, hipStream_t stream);
 // n matrices (1 <= n <= MAX_GROUP, none empty) in one launch; all share T and the step.
 hipError_t launch_fused_group(const Args *a, int n, int moment_kind, hipStream_t stream);
+// The fused step with update rule `epi` (any EpiKind but the store-G ones) on fp32 or bf16
+// state: n matrices (1 <= n <= MAX_GROUP, none empty) in one launch.
+hipError_t launch_fused_rule(const Args *a, int n, int epi, int moment_kind, hipStream_t stream);
 hipError_t launch_wgrad(const Args &a, int grad_f32, hipStream_t stream);
 hipError_t launch_adamw(const Args &a, int moment_kind, int grad_f32, hipStream_t stream);
 // dX = sum of dY_s W_s over n segments (0 <= n <= MAX_GROUP, none with d_out == 0; n == 0

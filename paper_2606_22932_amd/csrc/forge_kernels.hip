@@ -321,12 +321,151 @@ struct EpiMap {
     static constexpr int GS_BYTES = BP * GP * 4;
 };
 
-// AdamW on fp32 or bf16 moments.
-template <int BP, int BQ, int MK>
-struct EpiAdamW {
+// Per-element update rules of the fused step (the optimizer-family table of App. I; App. D
+// measures them by state count).  Each maps (g, w, s1, s2) to (w', s1', s2') in fp32 using
+// the scalars of Hyper; NS is the number of state tensors it reads and writes, and W_RW is
+// false for the rule that leaves the weight alone (Muon's momentum accumulate: the weight
+// update, a Newton--Schulz iteration over the whole buffer, reads state only and runs
+// elsewhere).  Decay: AdamW and Lion decay the weight directly (1 - lr wd); the others add
+// wd * w to the gradient first, as the common reference implementations do.
+template <int E> struct Rule;
+
+template <> struct Rule<EPI_ADAMW> {
+    static constexpr int NS = 2;
+    static constexpr bool W_RW = true;
+    static __device__ __forceinline__ void elem(float g, float w, float s1, float s2, const Hyper &h,
+                                                float &w1, float &t1, float &t2)
+    {
+        float rv;
+        adamw_elem(g, w, s1, s2, h, w1, t1, t2, rv);
+    }
+};
+
+template <> struct Rule<EPI_SGD> {            // w' = w - lr (g + wd w)
+    static constexpr int NS = 0;
+    static constexpr bool W_RW = true;
+    static __device__ __forceinline__ void elem(float g, float w, float, float, const Hyper &h,
+                                                float &w1, float &, float &)
+    {
+        const float gg = __builtin_fmaf(h.wd, w, g);
+        w1 = __builtin_fmaf(-h.lr, gg, w);
+    }
+};
+
+template <> struct Rule<EPI_SGDM> {           // b' = mu b + (g + wd w); w' = w - lr b'
+    static constexpr int NS = 1;
+    static constexpr bool W_RW = true;
+    static __device__ __forceinline__ void elem(float g, float w, float s1, float, const Hyper &h,
+                                                float &w1, float &t1, float &)
+    {
+        const float gg = __builtin_fmaf(h.wd, w, g);
+        t1 = __builtin_fmaf(h.b1, s1, gg);
+        w1 = __builtin_fmaf(-h.lr, t1, w);
+    }
+};
+
+template <> struct Rule<EPI_ADAGRAD> {        // s' = s + gg^2; w' = w - clr gg / (sqrt(s') + eps)
+    static constexpr int NS = 1;
+    static constexpr bool W_RW = true;
+    static __device__ __forceinline__ void elem(float g, float w, float s1, float, const Hyper &h,
+                                                float &w1, float &t1, float &)
+    {
+        const float gg = __builtin_fmaf(h.wd, w, g);
+        t1 = __builtin_fmaf(gg, gg, s1);
+        const float den = __builtin_amdgcn_sqrtf(t1) + h.eps;
+        w1 = __builtin_fmaf(-(h.lr * gg), __builtin_amdgcn_rcpf(den), w);
+    }
+};
+
+template <> struct Rule<EPI_RMSPROP> {        // v' = a v + (1-a) gg^2; w' = w - lr gg / (sqrt(v') + eps)
+    static constexpr int NS = 1;
+    static constexpr bool W_RW = true;
+    static __device__ __forceinline__ void elem(float g, float w, float s1, float, const Hyper &h,
+                                                float &w1, float &t1, float &)
+    {
+        const float gg = __builtin_fmaf(h.wd, w, g);
+        t1 = __builtin_fmaf(h.b2, s1, (h.c2 * gg) * gg);
+        const float den = __builtin_amdgcn_sqrtf(t1) + h.eps;
+        w1 = __builtin_fmaf(-(h.lr * gg), __builtin_amdgcn_rcpf(den), w);
+    }
+};
+
+template <> struct Rule<EPI_LION> {           // w' = (1 - lr wd) w - lr sign(b1 m + (1-b1) g); m' = b2 m + (1-b2) g
+    static constexpr int NS = 1;
+    static constexpr bool W_RW = true;
+    static __device__ __forceinline__ void elem(float g, float w, float s1, float, const Hyper &h,
+                                                float &w1, float &t1, float &)
+    {
+        const float c = __builtin_fmaf(h.b1, s1, h.c1 * g);
+        const float sg = c > 0.0f ? 1.0f : (c < 0.0f ? -1.0f : c);   // sign; 0 and NaN pass through
+        w1 = __builtin_fmaf(h.wdf, w, -(h.lr * sg));
+        t1 = __builtin_fmaf(h.b2, s1, h.c2 * g);
+    }
+};
+
+template <> struct Rule<EPI_NADAM> {          // Adam moments of gg; w' = w - (ka gg + kb m') / (sqrt(v'/bc2) + eps)
+    static constexpr int NS = 2;
+    static constexpr bool W_RW = true;
+    static __device__ __forceinline__ void elem(float g, float w, float s1, float s2, const Hyper &h,
+                                                float &w1, float &t1, float &t2)
+    {
+        const float gg = __builtin_fmaf(h.wd, w, g);
+        t1 = __builtin_fmaf(h.b1, s1, h.c1 * gg);
+        t2 = __builtin_fmaf(h.b2, s2, (h.c2 * gg) * gg);
+        const float den = __builtin_fmaf(__builtin_amdgcn_sqrtf(t2), h.inv_sqrt_bc2, h.eps);
+        const float num = __builtin_fmaf(h.ka, gg, h.kb * t1);
+        w1 = __builtin_fmaf(-num, __builtin_amdgcn_rcpf(den), w);
+    }
+};
+
+template <> struct Rule<EPI_RADAM> {          // Adam moments of gg; w' = w - ka m' / (sqrt(v') + eps) - kb m'
+    static constexpr int NS = 2;
+    static constexpr bool W_RW = true;
+    static __device__ __forceinline__ void elem(float g, float w, float s1, float s2, const Hyper &h,
+                                                float &w1, float &t1, float &t2)
+    {
+        const float gg = __builtin_fmaf(h.wd, w, g);
+        t1 = __builtin_fmaf(h.b1, s1, h.c1 * gg);
+        t2 = __builtin_fmaf(h.b2, s2, (h.c2 * gg) * gg);
+        const float den = __builtin_amdgcn_sqrtf(t2) + h.eps;
+        const float upd = __builtin_fmaf(h.ka * t1, __builtin_amdgcn_rcpf(den), h.kb * t1);
+        w1 = w - upd;
+    }
+};
+
+template <> struct Rule<EPI_ADAMAX> {         // m' = b1 m + (1-b1) gg; u' = max(b2 u, |gg| + eps); w' = w - lr/bc1 m'/u'
+    static constexpr int NS = 2;
+    static constexpr bool W_RW = true;
+    static __device__ __forceinline__ void elem(float g, float w, float s1, float s2, const Hyper &h,
+                                                float &w1, float &t1, float &t2)
+    {
+        const float gg = __builtin_fmaf(h.wd, w, g);
+        t1 = __builtin_fmaf(h.b1, s1, h.c1 * gg);
+        t2 = __builtin_fmaxf(h.b2 * s2, __builtin_fabsf(gg) + h.eps);
+        w1 = __builtin_fmaf(-(h.lr_bc1 * t1), __builtin_amdgcn_rcpf(t2), w);
+    }
+};
+
+template <> struct Rule<EPI_MUON> {           // B' = mu B + G (the GEMM's beta); W untouched
+    static constexpr int NS = 1;
+    static constexpr bool W_RW = false;
+    static __device__ __forceinline__ void elem(float g, float, float s1, float, const Hyper &h,
+                                                float &, float &t1, float &)
+    {
+        t1 = __builtin_fmaf(h.b1, s1, g);
+    }
+};
+
+// The epilogue of a rule on fp32 or bf16 state.  The stream waves prefetch the tile's
+// bf16 W and state into registers while the mainloop runs (fp32 state would not fit and
+// is loaded here); then each lane updates 8 consecutive columns of one row per pass.
+template <int BP, int BQ, int MK, int E>
+struct EpiRule {
     using M = EpiMap<BP, BQ>;
-    static constexpr bool PREFETCH = (MK == MK_BF16);   // fp32 state would not fit in registers
-    u32x4_t pw[PREFETCH ? M::NPASS : 1], pm[PREFETCH ? M::NPASS : 1], pv[PREFETCH ? M::NPASS : 1];
+    using R = Rule<E>;
+    static constexpr bool PREFETCH = (MK == MK_BF16);
+    static constexpr int NPF = PREFETCH ? M::NPASS : 1;
+    u32x4_t pw[R::W_RW ? NPF : 1], ps1[R::NS >= 1 ? NPF : 1], ps2[R::NS >= 2 ? NPF : 1];
 
     // Loads of pass I (one row per lane) into the prefetch registers.
     template <int I>
@@ -335,12 +474,15 @@ struct EpiAdamW {
         if constexpr (PREFETCH) {
             const int rs = s / M::LPR, q = q0 + (s % M::LPR) * 8;
             const int p = p0 + I * M::RPP + rs;
-            pw[I] = pm[I] = pv[I] = u32x4_t{0u, 0u, 0u, 0u};
+            const u32x4_t z = {0u, 0u, 0u, 0u};
+            if constexpr (R::W_RW) pw[I] = z;
+            if constexpr (R::NS >= 1) ps1[I] = z;
+            if constexpr (R::NS >= 2) ps2[I] = z;
             if (q < a.d_in && p < a.d_out) {
                 const size_t off = (size_t)p * a.d_in + q;
-                pw[I] = ld_nt<u32x4_t>(a.W + off);
-                pm[I] = ld_nt<u32x4_t>(static_cast<const uint16_t *>(a.m) + off);
-                pv[I] = ld_nt<u32x4_t>(static_cast<const uint16_t *>(a.v) + off);
+                if constexpr (R::W_RW) pw[I] = ld_nt<u32x4_t>(a.W + off);
+                if constexpr (R::NS >= 1) ps1[I] = ld_nt<u32x4_t>(static_cast<const uint16_t *>(a.m) + off);
+                if constexpr (R::NS >= 2) ps2[I] = ld_nt<u32x4_t>(static_cast<const uint16_t *>(a.v) + off);
             }
         }
     }
@@ -350,6 +492,42 @@ struct EpiAdamW {
     {
         prefetch_pass<I>(a, p0, q0, s);
         if constexpr (I + 1 < M::NPASS) prefetch<I + 1>(a, p0, q0, s);
+    }
+
+    // Element e of 8 consecutive values held as packed bf16 pairs, or as two fp32 quads.
+    static __device__ __forceinline__ float elt(const u32x4_t &u, int e)
+    {
+        return (e & 1) ? bf_hi(u[e >> 1]) : bf_lo(u[e >> 1]);
+    }
+    static __device__ __forceinline__ float elt(const f32x4_t &x0, const f32x4_t &x1, int e)
+    {
+        return e < 4 ? x0[e] : x1[e - 4];
+    }
+
+    static __device__ __forceinline__ void load_f32(const void *base, size_t off, bool ok, f32x4_t &x0,
+                                                    f32x4_t &x1)
+    {
+        x0 = f32x4_t{0, 0, 0, 0};
+        x1 = x0;
+        if (ok) {
+            const float *p = static_cast<const float *>(base) + off;
+            x0 = ld_nt<f32x4_t>(p);
+            x1 = ld_nt<f32x4_t>(p + 4);
+        }
+    }
+
+    static __device__ __forceinline__ void store_state(void *base, size_t off, const float (&f)[8])
+    {
+        if constexpr (MK == MK_BF16) {
+            u32x4_t u;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) u[k] = pack_bf16(f[2 * k], f[2 * k + 1]);
+            st_nt<u32x4_t>(static_cast<uint16_t *>(base) + off, u);
+        } else {
+            float *p = static_cast<float *>(base) + off;
+            st_nt<f32x4_t>(p, f32x4_t{f[0], f[1], f[2], f[3]});
+            st_nt<f32x4_t>(p + 4, f32x4_t{f[4], f[5], f[6], f[7]});
+        }
     }
 
     __device__ __forceinline__ void run(const Args &a, int p0, int q0, int s, const float *Gs)
@@ -364,67 +542,44 @@ struct EpiAdamW {
             const float *gr = Gs + (i * M::RPP + rs) * M::GP + qo;
             const f32x4_t g0 = *reinterpret_cast<const f32x4_t *>(gr);
             const f32x4_t g1 = *reinterpret_cast<const f32x4_t *>(gr + 4);
-            const float g[8] = {g0[0], g0[1], g0[2], g0[3], g1[0], g1[1], g1[2], g1[3]};
-            u32x4_t w4;
-            float mf[8], vf[8];
+            // W and the states stay packed until each element is needed
+            u32x4_t w4 = {0u, 0u, 0u, 0u}, a4 = w4, b4 = w4;
+            f32x4_t a0 = {0, 0, 0, 0}, a1 = a0, b0 = a0, b1 = a0;
             if constexpr (PREFETCH) {
-                w4 = pw[i];
-#pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    mf[2 * k] = bf_lo(pm[i][k]); mf[2 * k + 1] = bf_hi(pm[i][k]);
-                    vf[2 * k] = bf_lo(pv[i][k]); vf[2 * k + 1] = bf_hi(pv[i][k]);
-                }
+                if constexpr (R::W_RW) w4 = pw[i];
+                if constexpr (R::NS >= 1) a4 = ps1[i];
+                if constexpr (R::NS >= 2) b4 = ps2[i];
             } else {
-                w4 = u32x4_t{0u, 0u, 0u, 0u};
-                f32x4_t m0 = {0, 0, 0, 0}, m1 = m0, v0 = m0, v1 = m0;
-                if (ok) {
-                    w4 = ld_nt<u32x4_t>(a.W + off);
-                    const float *mp = static_cast<const float *>(a.m) + off;
-                    const float *vp = static_cast<const float *>(a.v) + off;
-                    m0 = ld_nt<f32x4_t>(mp); m1 = ld_nt<f32x4_t>(mp + 4);
-                    v0 = ld_nt<f32x4_t>(vp); v1 = ld_nt<f32x4_t>(vp + 4);
-                }
-#pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    mf[k] = m0[k]; mf[k + 4] = m1[k];
-                    vf[k] = v0[k]; vf[k + 4] = v1[k];
-                }
+                if constexpr (R::W_RW)
+                    if (ok) w4 = ld_nt<u32x4_t>(a.W + off);
+                if constexpr (R::NS >= 1) load_f32(a.m, off, ok, a0, a1);
+                if constexpr (R::NS >= 2) load_f32(a.v, off, ok, b0, b1);
             }
-            float wo[8], mo[8], vo[8];
+            float wo[8], o1[8], o2[8];
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                float rv;
-                adamw_elem(g[2 * k], bf_lo(w4[k]), mf[2 * k], vf[2 * k], h, wo[2 * k], mo[2 * k],
-                           vo[2 * k], rv);
-                adamw_elem(g[2 * k + 1], bf_hi(w4[k]), mf[2 * k + 1], vf[2 * k + 1], h,
-                           wo[2 * k + 1], mo[2 * k + 1], vo[2 * k + 1], rv);
+            for (int e = 0; e < 8; ++e) {
+                const float g = elt(g0, g1, e);
+                const float w = R::W_RW ? elt(w4, e) : 0.0f;
+                const float x = R::NS >= 1 ? (PREFETCH ? elt(a4, e) : elt(a0, a1, e)) : 0.0f;
+                const float y = R::NS >= 2 ? (PREFETCH ? elt(b4, e) : elt(b0, b1, e)) : 0.0f;
+                R::elem(g, w, x, y, h, wo[e], o1[e], o2[e]);
             }
             if (ok) {
-                u32x4_t wn;
+                if constexpr (R::W_RW) {
+                    u32x4_t wn;
 #pragma unroll
-                for (int k = 0; k < 4; ++k) wn[k] = pack_bf16(wo[2 * k], wo[2 * k + 1]);
-                st_nt<u32x4_t>(a.W + off, wn);
-                if constexpr (MK == MK_BF16) {
-                    u32x4_t mn, vn;
-#pragma unroll
-                    for (int k = 0; k < 4; ++k) {
-                        mn[k] = pack_bf16(mo[2 * k], mo[2 * k + 1]);
-                        vn[k] = pack_bf16(vo[2 * k], vo[2 * k + 1]);
-                    }
-                    st_nt<u32x4_t>(static_cast<uint16_t *>(a.m) + off, mn);
-                    st_nt<u32x4_t>(static_cast<uint16_t *>(a.v) + off, vn);
-                } else {
-                    float *mp = static_cast<float *>(a.m) + off;
-                    float *vp = static_cast<float *>(a.v) + off;
-                    st_nt<f32x4_t>(mp, f32x4_t{mo[0], mo[1], mo[2], mo[3]});
-                    st_nt<f32x4_t>(mp + 4, f32x4_t{mo[4], mo[5], mo[6], mo[7]});
-                    st_nt<f32x4_t>(vp, f32x4_t{vo[0], vo[1], vo[2], vo[3]});
-                    st_nt<f32x4_t>(vp + 4, f32x4_t{vo[4], vo[5], vo[6], vo[7]});
+                    for (int k = 0; k < 4; ++k) wn[k] = pack_bf16(wo[2 * k], wo[2 * k + 1]);
+                    st_nt<u32x4_t>(a.W + off, wn);
                 }
+                if constexpr (R::NS >= 1) store_state(a.m, off, o1);
+                if constexpr (R::NS >= 2) store_state(a.v, off, o2);
             }
         }
     }
 };
+
+template <int BP, int BQ, int MK>
+using EpiAdamW = EpiRule<BP, BQ, MK, EPI_ADAMW>;
 
 // AdamW on int8 block-absmax moments (App. B scheme; blocks of 256 rows along d_out,
 // second moment stored through its square root, codes of v floored at 1).  The tile is
@@ -632,8 +787,10 @@ __device__ __forceinline__ void epi_store_g(const Args &a, int p0, int q0, int s
 
 // ------------------------------------------------------------------------ kernels
 
+// At most 128 VGPRs (four waves per SIMD): two 512-thread workgroups per CU, one math and
+// one stream wave of each on every SIMD.  At 129-136 registers only one would fit.
 template <int BP, int BQ, int MK, int EPI>
-__global__ void __launch_bounds__(NT, 2) fused_kernel(GroupArgs g)
+__global__ void __launch_bounds__(NT, 4) fused_kernel(GroupArgs g)
 {
     static_assert(MK != MK_I8, "int8 moments run in pipelined_i8_kernel");
     using ML = Mainloop<BP, BQ, NSTAGE, TK128>;
@@ -661,8 +818,8 @@ __global__ void __launch_bounds__(NT, 2) fused_kernel(GroupArgs g)
         ml.run(a, p0, q0, smem, wave, lane);
         ml.template stage_g<EM::GP>(Gs, wave, lane);
         lds_barrier();
-    } else if constexpr (EPI == EPI_ADAMW) {
-        EpiAdamW<BP, BQ, MK> ep;
+    } else if constexpr (EPI != EPI_STORE_BF16 && EPI != EPI_STORE_F32) {
+        EpiRule<BP, BQ, MK, EPI> ep;
         ep.prefetch(a, p0, q0, s);
         for (int i = 0; i < nbar; ++i) lds_barrier();
         lds_barrier();
@@ -1174,6 +1331,30 @@ hipError_t launch_fused_group(const Args *a, int n, int mk, hipStream_t st)
     if (mk == MK_I8) return launch_i8_pipelined(a, n, st);
     if (mk == MK_BF16) return launch_group<BP_F, BQ_F, MK_BF16, EPI_ADAMW>(a, n, st);
     return launch_group<BP_F, BQ_F, MK_F32, EPI_ADAMW>(a, n, st);
+}
+
+template <int E>
+static hipError_t launch_rule(const Args *a, int n, int mk, hipStream_t st)
+{
+    if (mk == MK_BF16) return launch_group<BP_F, BQ_F, MK_BF16, E>(a, n, st);
+    return launch_group<BP_F, BQ_F, MK_F32, E>(a, n, st);
+}
+
+hipError_t launch_fused_rule(const Args *a, int n, int epi, int mk, hipStream_t st)
+{
+    switch (epi) {
+    case EPI_ADAMW: return launch_rule<EPI_ADAMW>(a, n, mk, st);
+    case EPI_SGD: return launch_rule<EPI_SGD>(a, n, mk, st);
+    case EPI_SGDM: return launch_rule<EPI_SGDM>(a, n, mk, st);
+    case EPI_ADAGRAD: return launch_rule<EPI_ADAGRAD>(a, n, mk, st);
+    case EPI_RMSPROP: return launch_rule<EPI_RMSPROP>(a, n, mk, st);
+    case EPI_LION: return launch_rule<EPI_LION>(a, n, mk, st);
+    case EPI_NADAM: return launch_rule<EPI_NADAM>(a, n, mk, st);
+    case EPI_RADAM: return launch_rule<EPI_RADAM>(a, n, mk, st);
+    case EPI_ADAMAX: return launch_rule<EPI_ADAMAX>(a, n, mk, st);
+    case EPI_MUON: return launch_rule<EPI_MUON>(a, n, mk, st);
+    default: return hipErrorInvalidValue;
+    }
 }
 
 hipError_t launch_fused(const Args &a, int mk, hipStream_t st)

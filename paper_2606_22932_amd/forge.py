@@ -21,8 +21,14 @@ STATUS = {
     0: "FORGE_OK", 1: "FORGE_ERR_NULL_POINTER", 2: "FORGE_ERR_INVALID_SHAPE",
     3: "FORGE_ERR_UNSUPPORTED_SHAPE", 4: "FORGE_ERR_INVALID_HYPERPARAM",
     5: "FORGE_ERR_INVALID_DTYPE", 6: "FORGE_ERR_MISALIGNED", 7: "FORGE_ERR_ALIASING",
-    8: "FORGE_ERR_NO_DEVICE", 9: "FORGE_ERR_LAUNCH",
+    8: "FORGE_ERR_NO_DEVICE", 9: "FORGE_ERR_LAUNCH", 10: "FORGE_ERR_INVALID_OPTIMIZER",
 }
+# forge_optimizer codes of include/forge.h
+OPTIMIZERS = {"adamw": 0, "sgd": 1, "sgd_momentum": 2, "adagrad": 3, "rmsprop": 4, "lion": 5, "nadam": 6,
+              "radam": 7, "adamax": 8, "muon_accumulate": 9}
+# state tensors each update rule reads and writes
+OPTIMIZER_STATES = {"adamw": 2, "sgd": 0, "sgd_momentum": 1, "adagrad": 1, "rmsprop": 1, "lion": 1, "nadam": 2,
+                    "radam": 2, "adamax": 2, "muon_accumulate": 1}
 HEADER = os.path.join(_build.ROOT, "include", "forge.h")
 
 
@@ -40,6 +46,12 @@ _P, _I64, _I32, _F = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_f
 FORGE_MAX_GROUP = 8
 
 
+class forge_hparams(ctypes.Structure):
+    """``forge_hparams`` of ``include/forge.h``."""
+    _fields_ = [("lr", _F), ("beta1", _F), ("beta2", _F), ("eps", _F), ("weight_decay", _F),
+                ("lr_decay", _F), ("momentum_decay", _F)]
+
+
 class forge_matrix(ctypes.Structure):
     """``forge_matrix`` of ``include/forge.h``: one matrix of a grouped step."""
     _fields_ = [("X", _P), ("dY", _P), ("W", _P), ("m", _P), ("v", _P), ("m_scale", _P),
@@ -50,6 +62,8 @@ _SIGS = {
     "forge_linear_step": [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I32, _F, _F, _F, _F, _F, _I64, _P],
     "forge_linear_step_grouped": [ctypes.POINTER(forge_matrix), _I32, _I64, _I32, _F, _F, _F, _F, _F,
                                   _I64, _P],
+    "forge_linear_step_opt": [_P, _P, _P, _P, _P, _I64, _I64, _I64, _I32, _I32, ctypes.POINTER(forge_hparams),
+                              _I64, _P],
     "forge_input_grad": [_P, _P, _P, _I64, _I64, _I64, _P],
     "forge_linear_backward": [_P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I32, _F, _F, _F, _F, _F,
                               _I64, _P],
@@ -163,6 +177,41 @@ def forge_linear_step(X, dY, W, m, v, m_scale=None, v_scale=None, *, lr, beta1, 
                                  _ptr(v_scale), T, d_in, d_out, _moment_code(m), lr, beta1, beta2,
                                  eps, weight_decay, int(step), _stream(stream, W))
     _check(st, "forge_linear_step")
+
+
+def forge_linear_step_opt(X, dY, W, s1=None, s2=None, *, optimizer, lr, beta1=0.0, beta2=0.0, eps=1e-8,
+                          weight_decay=0.0, lr_decay=0.0, momentum_decay=0.004, step, stream=None):
+    """The fused step with update rule ``optimizer`` (a key of OPTIMIZERS) on fp32 or bf16
+    state tensors s1, s2 (as many as the rule has).  W may be None for 'muon_accumulate'."""
+    import torch
+    if optimizer not in OPTIMIZERS:
+        raise ValueError(f"unknown optimizer {optimizer!r}; one of {sorted(OPTIMIZERS)}")
+    ns = OPTIMIZER_STATES[optimizer]
+    states = [t for t in (s1, s2)[:ns]]
+    if any(t is None for t in states):
+        raise ValueError(f"{optimizer} needs {ns} state tensor(s)")
+    _dev(X, dY, W, *states)
+    if X.dtype != torch.bfloat16 or dY.dtype != torch.bfloat16:
+        raise TypeError("X and dY must be bfloat16")
+    T, d_in = X.shape
+    T2, d_out = dY.shape
+    if T2 != T:
+        raise ValueError("X and dY disagree on T")
+    for t in ([W] if W is not None else []):
+        if t.dtype != torch.bfloat16 or tuple(t.shape) != (d_out, d_in):
+            raise ValueError("W must be bfloat16 [d_out, d_in]")
+    code = FORGE_MOMENT_BF16
+    if states:
+        code = _moment_code(states[0])
+        if code == FORGE_MOMENT_I8 or any(t.dtype != states[0].dtype or tuple(t.shape) != (d_out, d_in)
+                                          for t in states):
+            raise ValueError("state tensors must all be float32 or all bfloat16, [d_out, d_in]")
+    hp = forge_hparams(lr, beta1, beta2, eps, weight_decay, lr_decay, momentum_decay)
+    ref = W if W is not None else dY
+    st = lib().forge_linear_step_opt(_ptr(X), _ptr(dY), _ptr(W), _ptr(s1 if ns >= 1 else None),
+                                     _ptr(s2 if ns >= 2 else None), T, d_in, d_out, OPTIMIZERS[optimizer], code,
+                                     ctypes.byref(hp), int(step), _stream(stream, ref))
+    _check(st, "forge_linear_step_opt")
 
 
 def _group(mats):

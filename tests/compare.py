@@ -137,3 +137,77 @@ def check_step(gpu: dict, ora: dict, moment: str, w_frac: float = 0.999, hp: dic
         out["m"] = check_moment(gpu["m"], ora["m"], ora["m64"], moment, "m", wm)
         out["v"] = check_moment(gpu["v"], ora["v"], ora["v64"], moment, "v", wv)
     return out
+
+
+# ----------------------------------------------------------------------------- other update rules
+
+def rule_windows(opt: int, ora: dict, hp: dict, G: np.ndarray, EG: np.ndarray, W64: np.ndarray,
+                 s1: np.ndarray, s2: np.ndarray):
+    """Per-element bounds on the kernel's fp32 states of update rule `opt` (codes of the
+    oracle), as for AdamW: the gradient's accumulation error E_G carried through the rule's
+    recurrence, plus a few fp32 roundings of the terms (see moment_windows)."""
+    import oracle as o
+    f = lambda x: float(np.float32(x))
+    b1, b2, wd = f(hp.get("beta1", 0)), f(hp.get("beta2", 0)), f(hp.get("weight_decay", 0))
+    gg = G + wd * W64
+    a, b = (np.abs(x) if x is not None else 0.0 for x in (s1, s2))
+    E = EG
+    sq = 2 * np.abs(gg) * E + E * E
+    if opt in (o.OPT_SGD_MOMENTUM,):
+        return E + 4 * U32 * (b1 * a + 2 * np.abs(gg) + np.abs(wd * W64)), None
+    if opt == o.OPT_ADAGRAD:
+        return sq + 4 * U32 * (a + 2 * gg * gg), None
+    if opt == o.OPT_RMSPROP:
+        return (1 - b2) * sq + 4 * U32 * (b2 * a + 2 * (1 - b2) * gg * gg), None
+    if opt == o.OPT_LION:
+        return (1 - b2) * E + 4 * U32 * (b2 * a + 2 * (1 - b2) * np.abs(G)), None
+    if opt == o.OPT_MUON:
+        return E + 4 * U32 * (b1 * a + 2 * np.abs(G)), None
+    if opt in (o.OPT_NADAM, o.OPT_RADAM, o.OPT_ADAMAX):
+        w1 = (1 - b1) * E + 4 * U32 * (b1 * a + 2 * (1 - b1) * np.abs(gg) + np.abs(wd * W64))
+        if opt == o.OPT_ADAMAX:
+            w2 = E + 4 * U32 * (b2 * b + np.abs(gg) + f(hp.get("eps", 0)))
+        else:
+            w2 = (1 - b2) * sq + 4 * U32 * (b2 * b + 2 * (1 - b2) * gg * gg)
+        return w1, w2
+    return None, None
+
+
+def lion_ambiguous(ora: dict, hp: dict, G: np.ndarray, EG: np.ndarray, s1: np.ndarray) -> np.ndarray:
+    """Elements whose Lion sign argument c lies within its error bound of zero: there the
+    kernel's fp32 c may take the other sign, and W may differ by up to 2 lr."""
+    b1 = float(np.float32(hp["beta1"]))
+    win = (1 - b1) * EG + 4 * U32 * (b1 * np.abs(s1) + 2 * (1 - b1) * np.abs(G))
+    return np.abs(ora["aux"]) <= win
+
+
+def check_rule_step(gpu: dict, ora: dict, opt: int, kind: str, hp: dict, G, EG, W64, s1_in, s2_in,
+                    w_frac: float = 0.999):
+    """W within 1 bf16 ulp on >= w_frac of the elements (Lion: outside its sign ties, where W
+    must match one of the sign alternatives); states as check_moment with rule_windows."""
+    import oracle as o
+    out = {}
+    if opt == o.OPT_MUON:
+        assert np.array_equal(gpu["W"], ora["W"]), "W changed under the momentum accumulate"
+    elif opt == o.OPT_LION:
+        amb = lion_ambiguous(ora, hp, G, EG, s1_in)
+        out["W"] = check_weight(gpu["W"][~amb], ora["W"][~amb], frac=w_frac)
+        if amb.any():
+            lr, wd = float(np.float32(hp["lr"])), float(np.float32(hp["weight_decay"]))
+            base = W64[amb] * (1 - lr * wd)
+            keys = [bf16_key(o.f64_to_bf16_bits(base + d)) for d in (-lr, 0.0, lr)]
+            kg = bf16_key(gpu["W"][amb])
+            ok = np.zeros(kg.shape, bool)
+            for k in keys:
+                ok |= np.abs(kg - k) <= 1
+            assert ok.all(), f"W: {int((~ok).sum())} sign-tie elements match no sign alternative"
+        out["lion_sign_ties"] = int(amb.sum())
+    else:
+        out["W"] = check_weight(gpu["W"], ora["W"], frac=w_frac)
+    w1, w2 = rule_windows(opt, ora, hp, G, EG, W64, s1_in, s2_in)
+    ns = o.RULE_STATES[opt]
+    if ns >= 1:
+        out["s1"] = check_moment(gpu["s1"], ora["s1"], ora["s1_64"], kind, "s1", w1)
+    if ns >= 2:
+        out["s2"] = check_moment(gpu["s2"], ora["s2"], ora["s2_64"], kind, "s2", w2)
+    return out

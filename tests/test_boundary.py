@@ -308,3 +308,69 @@ def test_backward_valid_arguments_reach_the_device_check():
     m0 = _mat(0)
     assert call_backward_group([m0, _mat(1, X=m0.X, d_out=64), _mat(2, X=m0.X, d_out=0)]) == NODEV
     assert call_backward_group([_mat(0, d_out=0)]) == NODEV
+
+
+# ----------------------------------------------------------------------------- update rules
+
+INVOPT = 10
+OPT = forge.OPTIMIZERS
+
+
+def call_opt(opt="sgd_momentum", T=64, d_in=128, d_out=256, md=BF16, hp=None, step=1, **over):
+    a = dict(BASE)
+    a.update({k: v for k, v in over.items() if k in a})
+    h = forge.forge_hparams(1e-3, 0.9, 0.99, 1e-8, 0.01, 0.0, 0.004)
+    for k, v in (hp or {}).items():
+        setattr(h, k, v)
+    code = OPT[opt] if isinstance(opt, str) else opt
+    return lib().forge_linear_step_opt(a["X"], a["dY"], a["W"], a["m"], a["v"], T, d_in, d_out, code, md,
+                                       None if over.get("null_hp") else ctypes.byref(h), step, None)
+
+
+def test_opt_code_dtype_and_hp_errors():
+    assert call_opt(opt=99) == INVOPT
+    assert call_opt(opt=-1) == INVOPT
+    assert call_opt(md=I8) == DTYPE
+    assert call_opt(md=5) == DTYPE
+    assert call_opt(null_hp=True) == NULLP
+    assert call_opt(d_in=12) == UNSUP
+
+
+def test_opt_state_pointers_follow_the_rule():
+    assert call_opt("sgd_momentum", m=0) == NULLP
+    assert call_opt("nadam", v=0) == NULLP
+    assert call_opt("adamw", W=0) == NULLP
+    assert call_opt("sgd_momentum", m=BASE["m"] + 4) == MISAL
+    assert call_opt("lion", m=BASE["W"] + 64) == ALIAS
+    assert call_opt("radam", v=BASE["m"] + 16) == ALIAS
+    assert call_opt("adagrad", m=BASE["dY"]) == ALIAS
+    assert call_opt("muon_accumulate", m=BASE["X"] + 32) == ALIAS
+
+
+def test_opt_hyperparameters_checked_per_rule():
+    assert call_opt(step=0) == HYPER
+    assert call_opt(hp=dict(lr=-1.0)) == HYPER
+    assert call_opt(hp=dict(weight_decay=float("nan"))) == HYPER
+    assert call_opt("sgd_momentum", hp=dict(beta1=1.0)) == HYPER
+    assert call_opt("nadam", hp=dict(beta2=1.0)) == HYPER
+    assert call_opt("nadam", hp=dict(momentum_decay=-1.0)) == HYPER
+    assert call_opt("adagrad", hp=dict(lr_decay=-0.1)) == HYPER
+    assert call_opt("adagrad", hp=dict(eps=0.0)) == HYPER
+    assert call_opt("rmsprop", hp=dict(beta2=-0.5)) == HYPER
+    assert call_opt("lion", hp=dict(beta1=1.5)) == HYPER
+    assert call_opt("muon_accumulate", hp=dict(beta1=1.5)) == HYPER
+
+
+def test_opt_empty_is_a_noop():
+    assert call_opt(d_in=0) == OK
+    assert call_opt("sgd", d_out=0, W=0) == OK
+
+
+@pytest.mark.skipif(_gpu_visible(), reason="on a GPU machine a valid call would launch on fake pointers")
+def test_opt_valid_arguments_reach_the_device_check():
+    for name in OPT:
+        assert call_opt(name) == NODEV, name
+    # rules read only the fields and tensors they use
+    assert call_opt("sgd", m=0, v=0, hp=dict(beta1=5.0, eps=0.0)) == NODEV
+    assert call_opt("muon_accumulate", W=0, v=0, hp=dict(beta1=1.0)) == NODEV
+    assert call_opt("sgd_momentum", v=0, hp=dict(beta2=7.0)) == NODEV

@@ -438,3 +438,187 @@ def test_i8_step_weight_update_reads_unquantized_state():
     s = np.repeat(out8["m_scale"], 256, axis=0)[:d_out]
     assert np.all(np.abs(dec - out8["m64"]) <= s / 2 * (1 + 1e-5))
     assert np.all(np.abs(out8["qm"] - out8["m"]) <= 0.5 + 1e-6)
+
+
+# ------------------------------------------------------------------------- other update rules
+
+from oracle import (OPT_ADAGRAD, OPT_ADAMAX, OPT_LION, OPT_MUON, OPT_NADAM, OPT_RADAM, OPT_RMSPROP,  # noqa: E402
+                    OPT_SGD, OPT_SGD_MOMENTUM)
+
+RHP = dict(lr=f32(2e-3), beta1=f32(0.9), beta2=f32(0.99), eps=f32(1e-8), weight_decay=f32(0.05),
+           lr_decay=f32(0.01), momentum_decay=f32(0.004))
+
+
+def _rule_inputs(seed, d_out=10, d_in=16):
+    rng = np.random.default_rng(seed)
+    G = rng.standard_normal((d_out, d_in)) * 0.02
+    W = bf16_rand((d_out, d_in), 0.02, 60 + seed)
+    s1 = (rng.standard_normal((d_out, d_in)) * 1e-3).astype(np.float32)
+    s2 = np.abs(rng.standard_normal((d_out, d_in)) * 1e-4).astype(np.float32)
+    return G, W, s1, s2
+
+
+def _torch_param(W):
+    return torch.nn.Parameter(torch.from_numpy(oracle.bf16_bits_to_f64(W)))
+
+
+def _t(a):
+    return torch.from_numpy(np.asarray(a, dtype=np.float64).copy())
+
+
+def _torch_step(opt_code, W, G, s1, s2, step, h):
+    """The same step by torch.optim (fp64, foreach=False): returns (W, state1, state2)."""
+    p = _torch_param(W)
+    ts = lambda: torch.tensor(float(step - 1), dtype=torch.float64)
+    if opt_code == OPT_SGD:
+        o = torch.optim.SGD([p], lr=h["lr"], weight_decay=h["weight_decay"], foreach=False)
+        names = ()
+    elif opt_code == OPT_SGD_MOMENTUM:
+        o = torch.optim.SGD([p], lr=h["lr"], momentum=h["beta1"], weight_decay=h["weight_decay"], foreach=False)
+        o.state[p]["momentum_buffer"] = _t(s1)
+        names = ("momentum_buffer",)
+    elif opt_code == OPT_ADAGRAD:
+        o = torch.optim.Adagrad([p], lr=h["lr"], lr_decay=h["lr_decay"], weight_decay=h["weight_decay"],
+                                eps=h["eps"], foreach=False)
+        o.state[p].update(step=ts(), sum=_t(s1))
+        names = ("sum",)
+    elif opt_code == OPT_RMSPROP:
+        o = torch.optim.RMSprop([p], lr=h["lr"], alpha=h["beta2"], eps=h["eps"], weight_decay=h["weight_decay"],
+                                foreach=False)
+        o.state[p].update(step=ts(), square_avg=_t(s1))
+        names = ("square_avg",)
+    elif opt_code == OPT_NADAM:
+        kw = dict(lr=h["lr"], betas=(h["beta1"], h["beta2"]), eps=h["eps"], weight_decay=h["weight_decay"],
+                  momentum_decay=h["momentum_decay"], foreach=False)
+        # torch's own momentum-schedule product after step - 1 steps (it depends on the step only)
+        q = torch.nn.Parameter(torch.zeros(1, dtype=torch.float64))
+        oq = torch.optim.NAdam([q], **kw)
+        for _ in range(step - 1):
+            q.grad = torch.ones(1, dtype=torch.float64)
+            oq.step()
+        mu_product = oq.state[q]["mu_product"].clone() if step > 1 else torch.tensor(1.0, dtype=torch.float64)
+        o = torch.optim.NAdam([p], **kw)
+        o.state[p].update(step=ts(), mu_product=mu_product, exp_avg=_t(s1), exp_avg_sq=_t(s2))
+        names = ("exp_avg", "exp_avg_sq")
+    elif opt_code == OPT_RADAM:
+        o = torch.optim.RAdam([p], lr=h["lr"], betas=(h["beta1"], h["beta2"]), eps=h["eps"],
+                              weight_decay=h["weight_decay"], foreach=False)
+        o.state[p].update(step=ts(), exp_avg=_t(s1), exp_avg_sq=_t(s2))
+        names = ("exp_avg", "exp_avg_sq")
+    elif opt_code == OPT_ADAMAX:
+        o = torch.optim.Adamax([p], lr=h["lr"], betas=(h["beta1"], h["beta2"]), eps=h["eps"],
+                               weight_decay=h["weight_decay"], foreach=False)
+        o.state[p].update(step=ts(), exp_avg=_t(s1), exp_inf=_t(s2))
+        names = ("exp_avg", "exp_inf")
+    p.grad = torch.from_numpy(G.copy())
+    o.step()
+    st = [o.state[p][n].numpy() for n in names]
+    return p.detach().numpy(), (st + [None, None])[0], (st + [None, None])[1]
+
+
+@pytest.mark.parametrize("step", [1, 3, 100])
+@pytest.mark.parametrize("opt_code", [OPT_SGD, OPT_SGD_MOMENTUM, OPT_ADAGRAD, OPT_RMSPROP, OPT_NADAM, OPT_RADAM,
+                                      OPT_ADAMAX],
+                         ids=["sgd", "sgd_momentum", "adagrad", "rmsprop", "nadam", "radam", "adamax"])
+def test_rules_match_torch_optim_fp64(opt_code, step):
+    """torch.optim (fp64) is the reference implementation each family was checked against."""
+    G, W, s1, s2 = _rule_inputs(step + 10 * opt_code)
+    hp = dict(RHP)
+    if opt_code in (OPT_NADAM, OPT_RADAM):
+        hp["beta2"] = f32(0.999)     # RAdam's rectification switches on within the steps tested
+    out = oracle.rule_step(G, W, s1, s2, opt=opt_code, state_dtype=MOMENT_F32, step=step, **hp)
+    prev = torch.get_default_dtype()
+    torch.set_default_dtype(torch.float64)     # torch's scalar state (NAdam's product) in fp64 too
+    try:
+        wt, a, b = _torch_step(opt_code, W, G, s1, s2, step, hp)
+    finally:
+        torch.set_default_dtype(prev)
+    np.testing.assert_allclose(out["W64"], wt, rtol=1e-13, atol=1e-18)
+    if a is not None:
+        np.testing.assert_allclose(out["s1_64"], a, rtol=1e-13, atol=1e-20)
+    if b is not None:
+        np.testing.assert_allclose(out["s2_64"], b, rtol=1e-13, atol=1e-20)
+
+
+def test_radam_takes_both_branches():
+    """rho_t > 5 decides RAdam's rectification: off at t = 1, on at t = 100 (beta2 = 0.999)."""
+    G, W, s1, s2 = _rule_inputs(5)
+    hp = dict(RHP, beta2=f32(0.999), weight_decay=0.0)
+    a = oracle.rule_step(G, W, s1, s2, opt=OPT_RADAM, state_dtype=MOMENT_F32, step=1, **hp)
+    # unrectified: w' = w - lr m' / (1 - beta1)
+    w = oracle.bf16_bits_to_f64(W)
+    np.testing.assert_allclose(a["W64"], w - f32(2e-3) * a["s1_64"] / (1 - f32(0.9)), rtol=1e-14)
+    b = oracle.rule_step(G, W, s1, s2, opt=OPT_RADAM, state_dtype=MOMENT_F32, step=100, **hp)
+    assert not np.allclose(b["W64"], w - f32(2e-3) * b["s1_64"] / (1 - f32(0.9) ** 100), rtol=1e-6)
+
+
+def test_lion_zero_betas_is_sign_descent():
+    """beta1 = beta2 = 0: Lion is sign descent with decoupled decay, and m' = g."""
+    G, W, s1, _ = _rule_inputs(6)
+    G[0, :3] = 0.0
+    out = oracle.rule_step(G, W, s1, opt=OPT_LION, state_dtype=MOMENT_F32, step=7,
+                           **dict(RHP, beta1=0.0, beta2=0.0))
+    w = oracle.bf16_bits_to_f64(W)
+    lr, wd = f32(2e-3), f32(0.05)
+    np.testing.assert_allclose(out["W64"], w * (1 - lr * wd) - lr * np.sign(G), rtol=1e-15, atol=1e-20)
+    np.testing.assert_array_equal(out["s1_64"], G)
+
+
+def test_lion_update_magnitude_and_momentum_closed_form():
+    G, W, s1, _ = _rule_inputs(7)
+    out = oracle.rule_step(G, W, s1, opt=OPT_LION, state_dtype=MOMENT_F32, step=3, **RHP)
+    w = oracle.bf16_bits_to_f64(W)
+    lr, wd = f32(2e-3), f32(0.05)
+    # every weight moves by exactly lr beyond its decay (no element has c == 0 here)
+    np.testing.assert_allclose(np.abs(out["W64"] - w * (1 - lr * wd)), lr, rtol=1e-12)
+    # the sign follows the beta1 interpolation, not beta2's
+    m = s1.astype(np.float64)
+    assert np.array_equal(np.sign(w * (1 - lr * wd) - out["W64"]), np.sign(out["aux"]))
+    # constant gradient from m = 0: after k steps m_k = (1 - beta2^k) g (EMA closed form)
+    m = np.zeros_like(s1)
+    for _ in range(5):
+        m = oracle.rule_step(G, W, m, opt=OPT_LION, state_dtype=MOMENT_F32, step=1, **RHP)["s1"]
+    np.testing.assert_allclose(m, (1 - f32(0.99) ** 5) * G, rtol=1e-6)
+
+
+def test_lion_beta1_and_beta2_roles_on_exact_values():
+    W = to_bits([[1.0, 1.0]])
+    G = np.array([[-1.0, 1.0]])
+    m = np.array([[1.0, -1.0]], dtype=np.float32)
+    out = oracle.rule_step(G, W, m, opt=OPT_LION, state_dtype=MOMENT_F32, step=1,
+                           lr=0.25, beta1=0.25, beta2=0.75, weight_decay=0.0)
+    # c = 0.25 m + 0.75 g = (-0.5, 0.5): the sign of g wins; m' = 0.75 m + 0.25 g = (0.5, -0.5)
+    np.testing.assert_array_equal(out["W64"], [[1.25, 0.75]])
+    np.testing.assert_array_equal(out["s1_64"], [[0.5, -0.5]])
+
+
+def test_muon_accumulate_is_heavy_ball_buffer_and_leaves_w():
+    """B' = mu B + G is the heavy-ball recurrence of torch.optim.SGD's momentum buffer
+    (dampening 0, no decay); W is not touched."""
+    G, W, s1, _ = _rule_inputs(8)
+    out = oracle.rule_step(G, W, s1, opt=OPT_MUON, state_dtype=MOMENT_F32, step=4, lr=0.0, beta1=f32(0.95))
+    p = _torch_param(W)
+    o = torch.optim.SGD([p], lr=0.0, momentum=f32(0.95), foreach=False)
+    o.state[p]["momentum_buffer"] = _t(s1)
+    p.grad = torch.from_numpy(G.copy())
+    o.step()
+    np.testing.assert_allclose(out["s1_64"], o.state[p]["momentum_buffer"].numpy(), rtol=1e-15)
+    assert np.array_equal(out["W"], W)
+
+
+def test_muon_accumulate_over_micro_batches_is_the_whole_batch_gradient():
+    """Accumulating micro-batches with beta = mu, then 1, gives mu B + G over all tokens
+    (Prop. 1: G is additive over a partition of the token axis)."""
+    T, d_in, d_out = 48, 16, 8
+    X = bf16_rand((T, d_in), 1.0, 70)
+    dY = bf16_rand((T, d_out), 0.01, 71)
+    W = bf16_rand((d_out, d_in), 0.02, 72)
+    B = np.zeros((d_out, d_in), np.float32) + np.float32(0.5)
+    mu = f32(0.95)
+    b1 = oracle.rule_step(oracle.wgrad(X[:20], dY[:20]), W, B, opt=OPT_MUON, state_dtype=MOMENT_F32, step=1,
+                          lr=0.0, beta1=mu)["s1_64"]
+    b2 = oracle.rule_step(oracle.wgrad(X[20:], dY[20:]), W, b1.astype(np.float32), opt=OPT_MUON,
+                          state_dtype=MOMENT_F32, step=1, lr=0.0, beta1=1.0)["s1_64"]
+    want = mu * 0.5 + oracle.wgrad(X, dY)
+    # the first call's B' is rounded to fp32 before the second: allow that rounding
+    np.testing.assert_allclose(b2, want, rtol=2 ** -23, atol=2 ** -24 * np.abs(b1).max())
