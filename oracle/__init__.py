@@ -193,6 +193,19 @@ def adamw(G, W, m, v, *, moment_dtype, lr, beta1, beta2, eps, weight_decay, step
     return out
 
 
+def adamw_f64(G, W, m, v, *, lr, beta1, beta2, eps, weight_decay, step):
+    """Algorithm 1 on fp64 arrays with no rounding to any storage type: the reference the
+    fidelity experiment (App. E) measures weight error against.  Returns (W', m', v')."""
+    f = lambda x: float(np.float32(x))            # hyper-parameters as the GPU receives them
+    b1, b2, eta, ep, lam = f(beta1), f(beta2), f(lr), f(eps), f(weight_decay)
+    m1 = b1 * m + (1.0 - b1) * G
+    v1 = b2 * v + (1.0 - b2) * G * G
+    mhat = m1 / (1.0 - b1 ** step)
+    vhat = v1 / (1.0 - b2 ** step)
+    W1 = (1.0 - eta * lam) * W - eta * mhat / (np.sqrt(vhat) + ep)
+    return W1, m1, v1
+
+
 def rule_step(G, W, s1=None, s2=None, *, opt, state_dtype, lr, beta1=0.0, beta2=0.0, eps=1e-8,
               weight_decay=0.0, lr_decay=0.0, momentum_decay=0.004, step):
     """One step of update rule ``opt`` (not AdamW) on an fp64 gradient; inputs are not modified.

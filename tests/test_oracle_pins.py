@@ -622,3 +622,19 @@ def test_muon_accumulate_over_micro_batches_is_the_whole_batch_gradient():
     want = mu * 0.5 + oracle.wgrad(X, dY)
     # the first call's B' is rounded to fp32 before the second: allow that rounding
     np.testing.assert_allclose(b2, want, rtol=2 ** -23, atol=2 ** -24 * np.abs(b1).max())
+
+
+def test_unrounded_adamw_reference_equals_the_oracle_before_rounding():
+    """adamw_f64 (the fidelity experiment's reference, no storage rounding) computes the
+    same fp64 values as the C oracle's AdamW before it rounds them to storage."""
+    rng = np.random.default_rng(9)
+    G = rng.standard_normal((12, 20)) * 0.02
+    W = bf16_rand((12, 20), 0.02, 90)
+    m, v = _state(12, 20, MOMENT_F32, 91, warm=True)
+    for step in (1, 7):
+        ora = oracle.adamw(G, W, m, v, moment_dtype=MOMENT_F32, step=step, **HP)
+        W1, m1, v1 = oracle.adamw_f64(G, oracle.bf16_bits_to_f64(W), m.astype(np.float64), v.astype(np.float64),
+                                      step=step, **HP)
+        np.testing.assert_allclose(W1, ora["W64"], rtol=1e-15, atol=0)
+        np.testing.assert_allclose(m1, ora["m64"], rtol=1e-15, atol=0)
+        np.testing.assert_allclose(v1, ora["v64"], rtol=1e-15, atol=0)
