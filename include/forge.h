@@ -54,12 +54,19 @@ extern "C" {
 typedef enum {
     FORGE_MOMENT_F32 = 0,  /* fp32 m and v */
     FORGE_MOMENT_BF16 = 1, /* bf16 m and v (round-to-nearest-even stores) */
-    FORGE_MOMENT_I8 = 2    /* int8 codes with one fp32 absmax scale per 256 rows of d_out and
+    FORGE_MOMENT_I8 = 2,   /* int8 codes with one fp32 absmax scale per 256 rows of d_out and
                               per column: m = s_m * q_m, v = (s_v * q_v)^2 (the code stores
                               sqrt(v)); scales are [ceil(d_out/256), d_in] fp32.  The int8
                               block scheme follows App. B (re-quantised every step, second
                               moment kept away from zero: its codes are at least 1 in any
                               non-zero block). */
+    FORGE_MOMENT_I8_ROW64 = 3 /* the paper's own int8 layout (App. B): one fp32 absmax scale
+                              per 64 consecutive elements of a row (along d_in, a shorter last
+                              block when d_in is not a multiple of 64): m = s_m * q_m and
+                              v = s_v * q_v (v itself stored); scales are
+                              [d_out, ceil(d_in/64)] fp32; same rounding and v floor as above.
+                              forge_linear_step(_grouped), the backward calls and forge_adamw
+                              accept it; forge_linear_step_opt does not. */
 } forge_moment_dtype;
 
 /* Element type of a materialised gradient (only the two-kernel path stores one). */
@@ -86,7 +93,8 @@ typedef enum {
  *   dY       bf16 [T, d_out]           upstream gradient (may be NULL when T == 0)
  *   W        bf16 [d_out, d_in]        weight, in/out
  *   m, v     [d_out, d_in] moments in `moment_dtype` (int8: codes), in/out
- *   m_scale, v_scale   int8 only: fp32 [ceil(d_out/256), d_in], in/out; ignored otherwise
+ *   m_scale, v_scale   int8 only: fp32 scales in the layout of `moment_dtype`, in/out;
+ *            ignored otherwise
  *   step     t >= 1, the step being taken (bias corrections 1 - beta^t)
  *   lr, beta1, beta2, eps, weight_decay   AdamW hyper-parameters (Algorithm 1 notation
  *            eta, beta1, beta2, epsilon, lambda); decay is decoupled: W *= 1 - lr*wd.
@@ -109,7 +117,7 @@ typedef struct forge_matrix {
     const void *dY;           /* bf16 [T, d_out] (may be NULL when T == 0) */
     void *W;                  /* bf16 [d_out, d_in], in/out */
     void *m, *v;              /* [d_out, d_in] moments in the group's moment dtype, in/out */
-    float *m_scale, *v_scale; /* int8 only: fp32 [ceil(d_out/256), d_in], in/out */
+    float *m_scale, *v_scale; /* int8 only: fp32 scales of the moment dtype's layout, in/out */
     int64_t d_in, d_out;
 } forge_matrix;
 

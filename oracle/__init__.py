@@ -21,7 +21,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "forge_oracle.c")
 _LIB = os.path.join(_HERE, "libforge_oracle.so")
 
-MOMENT_F32, MOMENT_BF16, MOMENT_I8 = 0, 1, 2
+MOMENT_F32, MOMENT_BF16, MOMENT_I8, MOMENT_I8_ROW64 = 0, 1, 2, 3
+ROW_BLOCK = 64
 # Update rules (forge_oracle_rule_step); AdamW is ``adamw``.
 OPT_ADAMW, OPT_SGD, OPT_SGD_MOMENTUM, OPT_ADAGRAD, OPT_RMSPROP, OPT_LION = 0, 1, 2, 3, 4, 5
 OPT_NADAM, OPT_RADAM, OPT_ADAMAX, OPT_MUON = 6, 7, 8, 9
@@ -61,6 +62,11 @@ def _load():
             lib.forge_oracle_wgrad.restype = None
             lib.forge_oracle_f64_to_bf16_array.argtypes = [P, I64, P]
             lib.forge_oracle_f64_to_bf16_array.restype = None
+            lib.forge_oracle_quantize_i8_row64.argtypes = [P, I64, I64, I32, P, P, P]
+            lib.forge_oracle_quantize_i8_row64.restype = None
+            lib.forge_oracle_adamw_i8row.argtypes = [P, P, P, P, P, P, I64, I64, F32, F32, F32, F32, F32, I64,
+                                                     P, P, P, P, P]
+            lib.forge_oracle_adamw_i8row.restype = None
             lib.forge_oracle_input_grad.argtypes = [P, P, I64, I64, I64, P]
             lib.forge_oracle_input_grad.restype = None
             lib.forge_oracle_quantize_i8.argtypes = [P, I64, I64, I32, P, P]
@@ -150,6 +156,26 @@ def quantize_i8(x: np.ndarray, second_moment: bool):
     return codes, scales
 
 
+def quantize_i8_row64(x: np.ndarray, second_moment: bool):
+    """The paper's int8 layout (App. B): one scale per 64 consecutive elements of a row,
+    v quantised directly (no square root), its codes floored at 1 in non-zero blocks.
+    ``x`` fp64 [d_out, d_in] -> (codes int8 [d_out, d_in], scales fp32 [d_out, ceil(d_in/64)])."""
+    x = _c(x, np.float64)
+    d_out, d_in = x.shape
+    codes = np.empty((d_out, d_in), dtype=np.int8)
+    scales = np.empty((d_out, (d_in + ROW_BLOCK - 1) // ROW_BLOCK), dtype=np.float32)
+    _load().forge_oracle_quantize_i8_row64(_ptr(x), d_in, d_out, int(second_moment), _ptr(codes), _ptr(scales),
+                                           None)
+    return codes, scales
+
+
+def dequantize_i8_row64(codes: np.ndarray, scales: np.ndarray) -> np.ndarray:
+    """Decode the 64-wide row-block layout: x = s * q (for v as well: v is stored directly)."""
+    d_in = codes.shape[1]
+    s = np.repeat(scales.astype(np.float64), ROW_BLOCK, axis=1)[:, :d_in]
+    return s * codes.astype(np.float64)
+
+
 def dequantize_i8(codes: np.ndarray, scales: np.ndarray, second_moment: bool) -> np.ndarray:
     """Decode int8 moments to fp64: m = s*q, v = (s*q)^2 (the stored quantity is sqrt(v))."""
     d_out = codes.shape[0]
@@ -168,6 +194,9 @@ def adamw(G, W, m, v, *, moment_dtype, lr, beta1, beta2, eps, weight_decay, step
     """
     G = _c(G, np.float64)
     d_out, d_in = G.shape
+    if moment_dtype == MOMENT_I8_ROW64:
+        return _adamw_i8row(G, W, m, v, m_scale, v_scale, lr=lr, beta1=beta1, beta2=beta2, eps=eps,
+                            weight_decay=weight_decay, step=step, want_quotients=want_quotients)
     W = _c(W, np.uint16).copy()
     mdt = {MOMENT_F32: np.float32, MOMENT_BF16: np.uint16, MOMENT_I8: np.int8}[moment_dtype]
     m, v = _c(m, mdt).copy(), _c(v, mdt).copy()
@@ -229,6 +258,24 @@ def rule_step(G, W, s1=None, s2=None, *, opt, state_dtype, lr, beta1=0.0, beta2=
         float(beta1), float(beta2), float(eps), float(weight_decay), float(lr_decay), float(momentum_decay),
         int(step), _ptr(W64), _ptr(S1), _ptr(S2), _ptr(AUX))
     return dict(W=W, s1=s1, s2=s2, W64=W64, s1_64=S1, s2_64=S2, aux=AUX)
+
+
+def _adamw_i8row(G, W, m, v, m_scale, v_scale, *, lr, beta1, beta2, eps, weight_decay, step, want_quotients):
+    d_out, d_in = G.shape
+    W = _c(W, np.uint16).copy()
+    m, v = _c(m, np.int8).copy(), _c(v, np.int8).copy()
+    m_scale, v_scale = _c(m_scale, np.float32).copy(), _c(v_scale, np.float32).copy()
+    W64, m64, v64 = (np.empty((d_out, d_in), dtype=np.float64) for _ in range(3))
+    qm = qv = None
+    if want_quotients:
+        qm, qv = np.empty((d_out, d_in), np.float64), np.empty((d_out, d_in), np.float64)
+    _load().forge_oracle_adamw_i8row(_ptr(G), _ptr(W), _ptr(m), _ptr(v), _ptr(m_scale), _ptr(v_scale), d_in, d_out,
+                                     float(lr), float(beta1), float(beta2), float(eps), float(weight_decay), int(step),
+                                     _ptr(W64), _ptr(m64), _ptr(v64), _ptr(qm), _ptr(qv))
+    out = dict(W=W, m=m, v=v, m_scale=m_scale, v_scale=v_scale, W64=W64, m64=m64, v64=v64)
+    if qm is not None:
+        out.update(qm=qm, qv=qv)
+    return out
 
 
 def linear_step(X, dY, W, m, v, **kw):

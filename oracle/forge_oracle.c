@@ -29,6 +29,11 @@
  * Hyper-parameters arrive as the fp32 values the GPU receives; they are promoted
  * to fp64 here, so lr = 1e-3 means (double)(float)1e-3.
  *
+ * The paper's own int8 layout (App. B), forge_oracle_adamw_i8row: one scale per 64
+ * consecutive elements of a row (along d_in), a = max |x| over the block, s = a/127,
+ * code = round_half_even(x/s) clamped to [-127, 127], for m and for v itself (no square
+ * root), the v codes floored at 1 inside non-zero blocks; decision in fp32 as above.
+ *
  * Other update rules (forge_oracle_rule_step): the coordinate-wise optimizer families of
  * the paper's family table (App. I) and Muon's momentum accumulate (regime 2 of App. A).
  * The paper states that each was checked against its reference implementation and does
@@ -49,7 +54,8 @@
 
 #define ORACLE_I8_BLOCK 256
 
-enum { ORACLE_MOMENT_F32 = 0, ORACLE_MOMENT_BF16 = 1, ORACLE_MOMENT_I8 = 2 };
+enum { ORACLE_MOMENT_F32 = 0, ORACLE_MOMENT_BF16 = 1, ORACLE_MOMENT_I8 = 2, ORACLE_MOMENT_I8_ROW64 = 3 };
+#define ORACLE_ROW_BLOCK 64
 
 /* ---------------------------------------------------------------- bf16 helpers */
 
@@ -330,6 +336,64 @@ void forge_oracle_linear_step(const uint16_t *X, const uint16_t *dY, uint16_t *W
     forge_oracle_adamw(G, W, m, v, m_scale, v_scale, d_in, d_out, moment_dtype, lr, beta1,
                        beta2, eps, weight_decay, step, round_grad_to_bf16, W64, m64, v64, qm, qv);
     if (!G_out) free(G);
+}
+
+/* ------------------------------------------------------------- int8, 64-wide row blocks */
+
+/* Quantize row blocks: x fp64 [d_out, d_in] -> codes [d_out, d_in], scales [d_out, nb]. */
+void forge_oracle_quantize_i8_row64(const double *x, int64_t d_in, int64_t d_out, int second_moment,
+                                    int8_t *codes, float *scales, double *quot)
+{
+    const int64_t nb = (d_in + ORACLE_ROW_BLOCK - 1) / ORACLE_ROW_BLOCK;
+#pragma omp parallel for schedule(static)
+    for (int64_t p = 0; p < d_out; ++p)
+        for (int64_t b = 0; b < nb; ++b) {
+            const int64_t q0 = b * ORACLE_ROW_BLOCK;
+            const int64_t n = d_in - q0 < ORACLE_ROW_BLOCK ? d_in - q0 : ORACLE_ROW_BLOCK;
+            const int64_t k = p * d_in + q0;
+            scales[p * nb + b] = quantize_column(x + k, n, 1, second_moment, codes + k, 1, quot ? quot + k : NULL);
+        }
+}
+
+/*
+ * AdamW (Algorithm 1) with the moments in the 64-wide row-block int8 layout: decode
+ * m = s_m q_m and v = s_v q_v, update in fp64, W' from the unquantised m', v' (App. B: the
+ * update arithmetic stays in full precision), then re-quantise m' and v' per row block.
+ */
+void forge_oracle_adamw_i8row(const double *G, uint16_t *W, int8_t *m, int8_t *v, float *m_scale,
+                              float *v_scale, int64_t d_in, int64_t d_out, float lr, float beta1,
+                              float beta2, float eps, float weight_decay, int64_t step, double *W64,
+                              double *m64, double *v64, double *qm, double *qv)
+{
+    const double b1 = (double)beta1, b2 = (double)beta2;
+    const double eta = (double)lr, lam = (double)weight_decay, ep = (double)eps;
+    const double bc1 = 1.0 - pow(b1, (double)step);
+    const double bc2 = 1.0 - pow(b2, (double)step);
+    const double wdf = 1.0 - eta * lam;
+    const int64_t nb = (d_in + ORACLE_ROW_BLOCK - 1) / ORACLE_ROW_BLOCK;
+    double *mn = (double *)malloc(sizeof(double) * (size_t)(d_in * d_out > 0 ? d_in * d_out : 1));
+    double *vn = (double *)malloc(sizeof(double) * (size_t)(d_in * d_out > 0 ? d_in * d_out : 1));
+#pragma omp parallel for schedule(static)
+    for (int64_t k = 0; k < d_in * d_out; ++k) {
+        const int64_t p = k / d_in, q = k % d_in;
+        const double m0 = (double)m_scale[p * nb + q / ORACLE_ROW_BLOCK] * (double)m[k];
+        const double v0 = (double)v_scale[p * nb + q / ORACLE_ROW_BLOCK] * (double)v[k];
+        const double g = G[k];
+        const double m1 = b1 * m0 + (1.0 - b1) * g;
+        const double v1 = b2 * v0 + (1.0 - b2) * g * g;
+        const double w0 = forge_oracle_bf16_to_f64(W[k]);
+        const double w1 = wdf * w0 - eta * (m1 / bc1) / (sqrt(v1 / bc2) + ep);
+        W[k] = forge_oracle_f64_to_bf16(w1);
+        mn[k] = m1;
+        vn[k] = v1;
+        if (W64) W64[k] = w1;
+        if (m64) m64[k] = m1;
+        if (v64) v64[k] = v1;
+    }
+    forge_oracle_quantize_i8_row64(mn, d_in, d_out, 0, m, m_scale, qm);
+    forge_oracle_quantize_i8_row64(vn, d_in, d_out, 1, v, v_scale, qv);
+    free(mn);
+    free(vn);
 }
 
 /* ------------------------------------------------------------- other update rules */

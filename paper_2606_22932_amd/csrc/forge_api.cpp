@@ -32,11 +32,21 @@ bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 int64_t moment_bytes(int32_t md) { return md == FORGE_MOMENT_F32 ? 4 : md == FORGE_MOMENT_BF16 ? 2 : 1; }
 
+bool is_int8(int32_t md) { return md == FORGE_MOMENT_I8 || md == FORGE_MOMENT_I8_ROW64; }
+
+// Bytes of one int8 scale tensor of a [d_out, d_in] moment.
+int64_t scale_bytes(int32_t md, int64_t d_in, int64_t d_out)
+{
+    if (md == FORGE_MOMENT_I8_ROW64) return d_out * ((d_in + 63) / 64) * 4;
+    return ((d_out + 255) / 256) * d_in * 4;
+}
+
 bool finite(float x) { return std::isfinite(x); }
 
 forge_status check_dtype_moment(int32_t md)
 {
-    return (md == FORGE_MOMENT_F32 || md == FORGE_MOMENT_BF16 || md == FORGE_MOMENT_I8)
+    return (md == FORGE_MOMENT_F32 || md == FORGE_MOMENT_BF16 || md == FORGE_MOMENT_I8 ||
+            md == FORGE_MOMENT_I8_ROW64)
                ? FORGE_OK : FORGE_ERR_INVALID_DTYPE;
 }
 
@@ -96,7 +106,7 @@ forge_status check_state(void *W, void *m, void *v, float *ms, float *vs, int64_
                          int64_t d_out, int32_t md, StateSet &out)
 {
     if (!W || !m || !v) return FORGE_ERR_NULL_POINTER;
-    const bool i8 = (md == FORGE_MOMENT_I8);
+    const bool i8 = is_int8(md);
     if (i8 && (!ms || !vs)) return FORGE_ERR_NULL_POINTER;
     if (!aligned16(W) || !aligned16(m) || !aligned16(v)) return FORGE_ERR_MISALIGNED;
     if (i8 && (!aligned16(ms) || !aligned16(vs))) return FORGE_ERR_MISALIGNED;
@@ -106,7 +116,7 @@ forge_status check_state(void *W, void *m, void *v, float *ms, float *vs, int64_
     out.r[2] = range_of(v, moment_bytes(md) * P);
     out.n = 3;
     if (i8) {
-        const int64_t nsc = ((d_out + 255) / 256) * d_in * 4;
+        const int64_t nsc = scale_bytes(md, d_in, d_out);
         out.r[3] = range_of(ms, nsc);
         out.r[4] = range_of(vs, nsc);
         out.n = 5;

@@ -29,7 +29,7 @@ struct Args {
     const uint16_t *dY;    // bf16 [T, d_out]
     uint16_t *W;           // bf16 [d_out, d_in]
     void *m, *v;           // moments, storage per moment dtype
-    float *ms, *vs;        // int8 block scales [ceil(d_out/256), d_in]
+    float *ms, *vs;        // int8 block scales: [ceil(d_out/256), d_in], or [d_out, ceil(d_in/64)]
     void *G;               // materialised gradient (two-kernel path only)
     int T, d_in, d_out;
     int tiles_p, tiles_q;  // tile grid (along d_out, along d_in)
@@ -67,7 +67,10 @@ struct DxArgs {
     int group_t;           // raster group height in tiles
 };
 
-enum MomentKind { MK_F32 = 0, MK_BF16 = 1, MK_I8 = 2 };
+// Moment storage: fp32, bf16, int8 with one scale per 256 rows of a column (sqrt(v)
+// stored), int8 with one scale per 64 consecutive elements of a row (v stored).
+enum MomentKind { MK_F32 = 0, MK_BF16 = 1, MK_I8 = 2, MK_I8R64 = 3 };
+constexpr int I8_ROW_BLOCK = 64;
 // Tile epilogues of the fused kernel: the update rules (each a per-element function of G,
 // W and the rule's state), and the store-G control.
 enum EpiKind {

@@ -581,6 +581,116 @@ struct EpiRule {
 template <int BP, int BQ, int MK>
 using EpiAdamW = EpiRule<BP, BQ, MK, EPI_ADAMW>;
 
+// AdamW on int8 moments in the 64-wide row-block layout of App. B: one fp32 scale per 64
+// consecutive elements of a row, m = s_m q_m and v = s_v q_v (v stored itself).  A block is
+// exactly the 8 consecutive lanes that hold its row's 64 columns in one pass, so the new
+// block absmax closes with three xor shuffles and each row is dequantised, updated and
+// re-quantised in a single pass: s = absmax / 127 (fp32, correctly rounded),
+// q = round_half_even(x / s) clamped to [-127, 127], v codes at least 1 in a non-zero block.
+// The weight update reads the unquantised fp32 m', v'.
+template <int BP, int BQ>
+struct EpiI8Row {
+    using M = EpiMap<BP, BQ>;
+    static_assert(BQ % I8_ROW_BLOCK == 0 && M::LPR * 8 == BQ, "a block is 8 lanes of one row");
+    u32x4_t pw[M::NPASS];
+    u32x2_t pm[M::NPASS], pv[M::NPASS];
+    float sm[M::NPASS], sv[M::NPASS];
+
+    static __device__ __forceinline__ int nblocks(const Args &a) { return (a.d_in + I8_ROW_BLOCK - 1) / I8_ROW_BLOCK; }
+
+    template <int I>
+    __device__ __forceinline__ void prefetch_pass(const Args &a, int p0, int q0, int s)
+    {
+        const int rs = s / M::LPR, q = q0 + (s % M::LPR) * 8;
+        const int p = p0 + I * M::RPP + rs;
+        pw[I] = u32x4_t{0u, 0u, 0u, 0u};
+        pm[I] = pv[I] = u32x2_t{0u, 0u};
+        sm[I] = sv[I] = 0.0f;
+        if (q < a.d_in && p < a.d_out) {
+            const size_t off = (size_t)p * a.d_in + q;
+            const size_t so = (size_t)p * nblocks(a) + q / I8_ROW_BLOCK;
+            pw[I] = ld_nt<u32x4_t>(a.W + off);
+            pm[I] = ld_nt<u32x2_t>(static_cast<const int8_t *>(a.m) + off);
+            pv[I] = ld_nt<u32x2_t>(static_cast<const int8_t *>(a.v) + off);
+            sm[I] = a.ms[so];
+            sv[I] = a.vs[so];
+        }
+    }
+
+    template <int I = 0>
+    __device__ __forceinline__ void prefetch(const Args &a, int p0, int q0, int s)
+    {
+        prefetch_pass<I>(a, p0, q0, s);
+        if constexpr (I + 1 < M::NPASS) prefetch<I + 1>(a, p0, q0, s);
+    }
+
+    static __device__ __forceinline__ float code_at(u32x2_t c, int e)
+    {
+        return (float)(int8_t)((c[e >> 2] >> (8 * (e & 3))) & 0xFFu);
+    }
+
+    __device__ __forceinline__ void run(const Args &a, int p0, int q0, int s, const float *Gs)
+    {
+        const int rs = s / M::LPR, qo = (s % M::LPR) * 8, q = q0 + qo;
+        const Hyper h = a.h;
+#pragma unroll
+        for (int i = 0; i < M::NPASS; ++i) {
+            const int p = p0 + i * M::RPP + rs;
+            const bool ok = q < a.d_in && p < a.d_out;
+            const float *gr = Gs + (i * M::RPP + rs) * M::GP + qo;
+            const f32x4_t g0 = *reinterpret_cast<const f32x4_t *>(gr);
+            const f32x4_t g1 = *reinterpret_cast<const f32x4_t *>(gr + 4);
+            float wo[8], mo[8], vo[8];
+            float am = 0.0f, av = 0.0f;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const float g = e < 4 ? g0[e] : g1[e - 4];
+                const float w = (e & 1) ? bf_hi(pw[i][e >> 1]) : bf_lo(pw[i][e >> 1]);
+                float rv;
+                adamw_elem(g, w, sm[i] * code_at(pm[i], e), sv[i] * code_at(pv[i], e), h, wo[e], mo[e], vo[e], rv);
+                am = fmaxf(am, fabsf(mo[e]));
+                av = fmaxf(av, vo[e]);
+            }
+            if (!ok) am = av = 0.0f;
+#pragma unroll
+            for (int d = 1; d < 8; d <<= 1) {
+                am = fmaxf(am, __shfl_xor(am, d));
+                av = fmaxf(av, __shfl_xor(av, d));
+            }
+            const float scm = am / 127.0f, scv = av / 127.0f;
+            const float rcm = scm > 0.0f ? __builtin_amdgcn_rcpf(scm) : 0.0f;
+            const float rcv = scv > 0.0f ? __builtin_amdgcn_rcpf(scv) : 0.0f;
+            uint32_t cm[2] = {0u, 0u}, cv[2] = {0u, 0u};
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const float qm = fminf(fmaxf(__builtin_rintf(mo[e] * rcm), -127.0f), 127.0f);
+                float qv = fminf(fmaxf(__builtin_rintf(vo[e] * rcv), 1.0f), 127.0f);
+                if (!(rcv > 0.0f)) qv = 0.0f;
+                cm[e >> 2] |= ((uint32_t)(int32_t)qm & 0xFFu) << (8 * (e & 3));
+                cv[e >> 2] |= ((uint32_t)(int32_t)qv & 0xFFu) << (8 * (e & 3));
+            }
+            if (ok) {
+                const size_t off = (size_t)p * a.d_in + q;
+                u32x4_t wn;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) wn[k] = pack_bf16(wo[2 * k], wo[2 * k + 1]);
+                st_nt<u32x4_t>(a.W + off, wn);
+                st_nt<u32x2_t>(static_cast<int8_t *>(a.m) + off, u32x2_t{cm[0], cm[1]});
+                st_nt<u32x2_t>(static_cast<int8_t *>(a.v) + off, u32x2_t{cv[0], cv[1]});
+                if ((s & 7) == 0) {
+                    const size_t so = (size_t)p * nblocks(a) + q / I8_ROW_BLOCK;
+                    a.ms[so] = scm;
+                    a.vs[so] = scv;
+                }
+            }
+        }
+    }
+};
+
+// The epilogue of (moment kind, rule): the row-block int8 layout has its own (AdamW only).
+template <int BP, int BQ, int MK, int E> struct EpiSel { using T = EpiRule<BP, BQ, MK, E>; };
+template <int BP, int BQ> struct EpiSel<BP, BQ, MK_I8R64, EPI_ADAMW> { using T = EpiI8Row<BP, BQ>; };
+
 // AdamW on int8 block-absmax moments (App. B scheme; blocks of 256 rows along d_out,
 // second moment stored through its square root, codes of v floored at 1).  The tile is
 // one block tall, so each column's absmax is a reduction over the tile's 256 rows:
@@ -793,6 +903,8 @@ template <int BP, int BQ, int MK, int EPI>
 __global__ void __launch_bounds__(NT, 4) fused_kernel(GroupArgs g)
 {
     static_assert(MK != MK_I8, "int8 moments run in pipelined_i8_kernel");
+    static_assert(MK != MK_I8R64 || EPI == EPI_ADAMW || EPI == EPI_STORE_BF16 || EPI == EPI_STORE_F32,
+                  "row-block int8 moments: AdamW only");
     using ML = Mainloop<BP, BQ, NSTAGE, TK128>;
     using EM = EpiMap<BP, BQ>;
     constexpr int MAIN = ML::LDS_BYTES > EM::GS_BYTES ? ML::LDS_BYTES : EM::GS_BYTES;
@@ -819,7 +931,7 @@ __global__ void __launch_bounds__(NT, 4) fused_kernel(GroupArgs g)
         ml.template stage_g<EM::GP>(Gs, wave, lane);
         lds_barrier();
     } else if constexpr (EPI != EPI_STORE_BF16 && EPI != EPI_STORE_F32) {
-        EpiRule<BP, BQ, MK, EPI> ep;
+        typename EpiSel<BP, BQ, MK, EPI>::T ep;
         ep.prefetch(a, p0, q0, s);
         for (int i = 0; i < nbar; ++i) lds_barrier();
         lds_barrier();
@@ -873,7 +985,7 @@ __global__ void __launch_bounds__(NROLE, 2) adamw_kernel(Args a)
         lds_barrier();
         ep.run(a, p0, q0, s, Gs, red);
     } else {
-        EpiAdamW<BP, BQ, MK> ep;
+        typename EpiSel<BP, BQ, MK, EPI_ADAMW>::T ep;
         ep.prefetch(a, p0, q0, s);
         stage();
         lds_barrier();
@@ -1329,6 +1441,7 @@ static hipError_t launch_i8_pipelined(const Args *a, int n, hipStream_t st)
 hipError_t launch_fused_group(const Args *a, int n, int mk, hipStream_t st)
 {
     if (mk == MK_I8) return launch_i8_pipelined(a, n, st);
+    if (mk == MK_I8R64) return launch_group<BP_F, BQ_F, MK_I8R64, EPI_ADAMW>(a, n, st);
     if (mk == MK_BF16) return launch_group<BP_F, BQ_F, MK_BF16, EPI_ADAMW>(a, n, st);
     return launch_group<BP_F, BQ_F, MK_F32, EPI_ADAMW>(a, n, st);
 }
@@ -1377,6 +1490,12 @@ hipError_t launch_adamw(const Args &a0, int mk, int grad_f32, hipStream_t st)
             hipLaunchKernelGGL((adamw_kernel<BP_I8, BQ_I8, MK_I8, true>), dim3(n), dim3(NROLE), 0, st, a);
         else
             hipLaunchKernelGGL((adamw_kernel<BP_I8, BQ_I8, MK_I8, false>), dim3(n), dim3(NROLE), 0, st, a);
+    } else if (mk == MK_I8R64) {
+        Args a = with_grid(a0, BP_F, BQ_F, n);
+        if (grad_f32)
+            hipLaunchKernelGGL((adamw_kernel<BP_F, BQ_F, MK_I8R64, true>), dim3(n), dim3(NROLE), 0, st, a);
+        else
+            hipLaunchKernelGGL((adamw_kernel<BP_F, BQ_F, MK_I8R64, false>), dim3(n), dim3(NROLE), 0, st, a);
     } else if (mk == MK_BF16) {
         Args a = with_grid(a0, BP_F, BQ_F, n);
         if (grad_f32)

@@ -14,7 +14,7 @@ import threading
 
 from . import build as _build
 
-FORGE_MOMENT_F32, FORGE_MOMENT_BF16, FORGE_MOMENT_I8 = 0, 1, 2
+FORGE_MOMENT_F32, FORGE_MOMENT_BF16, FORGE_MOMENT_I8, FORGE_MOMENT_I8_ROW64 = 0, 1, 2, 3
 FORGE_GRAD_BF16, FORGE_GRAD_F32 = 0, 1
 
 STATUS = {
@@ -132,12 +132,24 @@ def _stream(stream, ref):
     return ctypes.c_void_p(torch.cuda.current_stream(ref.device).cuda_stream)
 
 
-def _moment_code(m):
+def _moment_code(m, m_scale=None):
+    """Moment dtype code; int8 moments name their layout through the scale tensor's shape:
+    [ceil(d_out/256), d_in] (256-row column blocks) or [d_out, ceil(d_in/64)] (64-wide row
+    blocks)."""
     import torch
-    codes = {torch.float32: FORGE_MOMENT_F32, torch.bfloat16: FORGE_MOMENT_BF16, torch.int8: FORGE_MOMENT_I8}
-    if m.dtype not in codes:
+    codes = {torch.float32: FORGE_MOMENT_F32, torch.bfloat16: FORGE_MOMENT_BF16}
+    if m.dtype in codes:
+        return codes[m.dtype]
+    if m.dtype != torch.int8:
         raise TypeError(f"moments must be float32, bfloat16 or int8, got {m.dtype}")
-    return codes[m.dtype]
+    if m_scale is None:
+        raise ValueError("int8 moments need their scale tensors")
+    d_out, d_in = m.shape
+    if tuple(m_scale.shape) == ((d_out + 255) // 256, d_in):
+        return FORGE_MOMENT_I8
+    if tuple(m_scale.shape) == (d_out, (d_in + 63) // 64):
+        return FORGE_MOMENT_I8_ROW64
+    raise ValueError(f"int8 scale shape {tuple(m_scale.shape)} matches neither layout for moments {tuple(m.shape)}")
 
 
 def _grad_code(G):
@@ -174,7 +186,7 @@ def forge_linear_step(X, dY, W, m, v, m_scale=None, v_scale=None, *, lr, beta1, 
     _dev(X, dY, W, m, v, m_scale, v_scale)
     T, d_in, d_out = _shapes(X, dY, W)
     st = lib().forge_linear_step(_ptr(X), _ptr(dY), _ptr(W), _ptr(m), _ptr(v), _ptr(m_scale),
-                                 _ptr(v_scale), T, d_in, d_out, _moment_code(m), lr, beta1, beta2,
+                                 _ptr(v_scale), T, d_in, d_out, _moment_code(m, m_scale), lr, beta1, beta2,
                                  eps, weight_decay, int(step), _stream(stream, W))
     _check(st, "forge_linear_step")
 
@@ -202,8 +214,10 @@ def forge_linear_step_opt(X, dY, W, s1=None, s2=None, *, optimizer, lr, beta1=0.
             raise ValueError("W must be bfloat16 [d_out, d_in]")
     code = FORGE_MOMENT_BF16
     if states:
+        if states[0].dtype == torch.int8:
+            raise ValueError("forge_linear_step_opt takes float32 or bfloat16 state")
         code = _moment_code(states[0])
-        if code == FORGE_MOMENT_I8 or any(t.dtype != states[0].dtype or tuple(t.shape) != (d_out, d_in)
+        if any(t.dtype != states[0].dtype or tuple(t.shape) != (d_out, d_in)
                                           for t in states):
             raise ValueError("state tensors must all be float32 or all bfloat16, [d_out, d_in]")
     hp = forge_hparams(lr, beta1, beta2, eps, weight_decay, lr_decay, momentum_decay)
@@ -224,7 +238,7 @@ def _group(mats):
     for i, (X, dY, W, m, v, ms, vs) in enumerate(mats):
         _dev(X, dY, W, m, v, ms, vs)
         Ti, d_in, d_out = _shapes(X, dY, W)
-        ci = _moment_code(m)
+        ci = _moment_code(m, ms)
         if T is None:
             T, code = Ti, ci
         elif Ti != T or ci != code:
@@ -276,7 +290,7 @@ def forge_linear_backward(X, dY, W, m, v, m_scale=None, v_scale=None, *, dX, lr,
     T, d_in, d_out = _shapes(X, dY, W)
     _dx(dX, T, d_in)
     st = lib().forge_linear_backward(_ptr(X), _ptr(dY), _ptr(W), _ptr(m), _ptr(v), _ptr(m_scale),
-                                     _ptr(v_scale), _ptr(dX), T, d_in, d_out, _moment_code(m), lr, beta1,
+                                     _ptr(v_scale), _ptr(dX), T, d_in, d_out, _moment_code(m, m_scale), lr, beta1,
                                      beta2, eps, weight_decay, int(step), _stream(stream, W))
     _check(st, "forge_linear_backward")
 
@@ -311,7 +325,7 @@ def forge_adamw(G, W, m, v, m_scale=None, v_scale=None, *, lr, beta1, beta2, eps
     if tuple(G.shape) != (d_out, d_in):
         raise ValueError("G must match W")
     st = lib().forge_adamw(_ptr(G), _grad_code(G), _ptr(W), _ptr(m), _ptr(v), _ptr(m_scale),
-                           _ptr(v_scale), d_in, d_out, _moment_code(m), lr, beta1, beta2, eps,
+                           _ptr(v_scale), d_in, d_out, _moment_code(m, m_scale), lr, beta1, beta2, eps,
                            weight_decay, int(step), _stream(stream, W))
     _check(st, "forge_adamw")
 
@@ -325,6 +339,6 @@ def forge_linear_step_unfused(X, dY, W, m, v, m_scale=None, v_scale=None, *, G_w
         raise ValueError("G_ws too small")
     st = lib().forge_linear_step_unfused(_ptr(X), _ptr(dY), _ptr(W), _ptr(m), _ptr(v),
                                          _ptr(m_scale), _ptr(v_scale), T, d_in, d_out,
-                                         _moment_code(m), lr, beta1, beta2, eps, weight_decay,
+                                         _moment_code(m, m_scale), lr, beta1, beta2, eps, weight_decay,
                                          int(step), _ptr(G_ws), _grad_code(G_ws), _stream(stream, W))
     _check(st, "forge_linear_step_unfused")

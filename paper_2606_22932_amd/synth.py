@@ -136,20 +136,28 @@ def warm_moments(mat: Matrix, wl: Workload, device="cpu", dtype=torch.float32):
     return m, v
 
 
-def random_i8_state(mat: Matrix, wl: Workload, device="cpu"):
+def random_i8_state(mat: Matrix, wl: Workload, device="cpu", layout="col256"):
     """Random int8 moment codes and positive fp32 scales of warm-state magnitude.
 
     Used where only the cost of a step matters (timing): the codes are uniform, m in
-    [-127, 127] and sqrt(v) in [1, 127]; scales are m_std*3/127 and sqrt(v_std)*3/127.
+    [-127, 127] and the second-moment code in [1, 127]; scales are m_std*3/127 and, for the
+    256-row column layout (which stores sqrt(v)), sqrt(v_std)*3/127, for the 64-wide row
+    layout (which stores v) v_std*3/127.  Scales are [ceil(d_out/256), d_in] (col256) or
+    [d_out, ceil(d_in/64)] (row64).
     """
     g = torch.Generator(device=device)
     g.manual_seed(seed_of(mat.base, 5))
     shape = (mat.d_out, mat.d_in)
-    nb = (mat.d_out + 255) // 256
     mq = torch.randint(-127, 128, shape, generator=g, device=device, dtype=torch.int8)
     vq = torch.randint(1, 128, shape, generator=g, device=device, dtype=torch.int8)
-    ms = torch.full((nb, mat.d_in), wl.m_std * 3 / 127, device=device, dtype=torch.float32)
-    vs = torch.full((nb, mat.d_in), (wl.v_std ** 0.5) * 3 / 127, device=device, dtype=torch.float32)
+    if layout == "col256":
+        sshape = ((mat.d_out + 255) // 256, mat.d_in)
+        v_scale = (wl.v_std ** 0.5) * 3 / 127
+    else:
+        sshape = (mat.d_out, (mat.d_in + 63) // 64)
+        v_scale = wl.v_std * 3 / 127
+    ms = torch.full(sshape, wl.m_std * 3 / 127, device=device, dtype=torch.float32)
+    vs = torch.full(sshape, v_scale, device=device, dtype=torch.float32)
     return mq, vq, ms, vs
 
 

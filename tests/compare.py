@@ -133,6 +133,19 @@ def check_step(gpu: dict, ora: dict, moment: str, w_frac: float = 0.999, hp: dic
         out["v"] = check_codes(gpu["v"], ora["v"], ora["qv"], "v codes", qwv)
         out["m_scale"] = check_scales(gpu["m_scale"], ora["m_scale"], "m scales")
         out["v_scale"] = check_scales(gpu["v_scale"], ora["v_scale"], "v scales")
+    elif moment == "i8r64":
+        qwm = qwv = None
+        if wm is not None:
+            d_in = gpu["m"].shape[1]
+            sm = np.repeat(ora["m_scale"].astype(np.float64), 64, axis=1)[:, :d_in]
+            sv = np.repeat(ora["v_scale"].astype(np.float64), 64, axis=1)[:, :d_in]
+            with np.errstate(divide="ignore", invalid="ignore"):
+                qwm = np.where(sm > 0, wm / sm, 0.0)
+                qwv = np.where(sv > 0, wv / sv, 0.0)        # v itself is quantised
+        out["m"] = check_codes(gpu["m"], ora["m"], ora["qm"], "m codes", qwm)
+        out["v"] = check_codes(gpu["v"], ora["v"], ora["qv"], "v codes", qwv)
+        out["m_scale"] = check_scales(gpu["m_scale"], ora["m_scale"], "m scales")
+        out["v_scale"] = check_scales(gpu["v_scale"], ora["v_scale"], "v scales")
     else:
         out["m"] = check_moment(gpu["m"], ora["m"], ora["m64"], moment, "m", wm)
         out["v"] = check_moment(gpu["v"], ora["v"], ora["v64"], moment, "v", wv)

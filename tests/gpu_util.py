@@ -14,7 +14,8 @@ import oracle
 from paper_2606_22932_amd import forge, synth
 
 HP = dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.1)
-MOMENT_CODE = {"f32": oracle.MOMENT_F32, "bf16": oracle.MOMENT_BF16, "i8": oracle.MOMENT_I8}
+MOMENT_CODE = {"f32": oracle.MOMENT_F32, "bf16": oracle.MOMENT_BF16, "i8": oracle.MOMENT_I8,
+               "i8r64": oracle.MOMENT_I8_ROW64}
 
 
 def bits(t: torch.Tensor) -> np.ndarray:
@@ -67,9 +68,12 @@ def make_problem(T, d_in, d_out, moment, seed, *, warm=True, x_std=1.0, dy_std=1
         p.m, p.v = bits(m), bits(v)
     elif moment == "bf16":
         p.m, p.v = bits(m.to(torch.bfloat16)), bits(v.to(torch.bfloat16))
-    else:
+    elif moment == "i8":
         p.m, p.m_scale = oracle.quantize_i8(m.double().numpy(), second_moment=False)
         p.v, p.v_scale = oracle.quantize_i8(v.double().numpy(), second_moment=True)
+    else:
+        p.m, p.m_scale = oracle.quantize_i8_row64(m.double().numpy(), second_moment=False)
+        p.v, p.v_scale = oracle.quantize_i8_row64(v.double().numpy(), second_moment=True)
     return p
 
 

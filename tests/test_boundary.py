@@ -64,12 +64,13 @@ def test_query_tile():
     assert forge.forge_query_tile(BF16)[0] % 8 == 0
     rows, cols, tk = forge.forge_query_tile(I8)
     assert rows == 256            # an int8 tile is exactly one scale block tall
+    assert forge.forge_query_tile(3)[1] % 64 == 0   # row-block int8: whole 64-wide blocks per tile
     r = ctypes.c_int32()
     assert lib().forge_query_tile(7, ctypes.byref(r), None, None) == DTYPE
 
 
 def test_dtype_errors():
-    assert call_step(md=3) == DTYPE
+    assert call_step(md=4) == DTYPE
     assert call_step(md=-1) == DTYPE
     assert call_unfused(gd=2) == DTYPE
     assert lib().forge_wgrad(BASE["X"], BASE["dY"], BASE["G"], 8, 8, 8, 5, None) == DTYPE
@@ -374,3 +375,27 @@ def test_opt_valid_arguments_reach_the_device_check():
     assert call_opt("sgd", m=0, v=0, hp=dict(beta1=5.0, eps=0.0)) == NODEV
     assert call_opt("muon_accumulate", W=0, v=0, hp=dict(beta1=1.0)) == NODEV
     assert call_opt("sgd_momentum", v=0, hp=dict(beta2=7.0)) == NODEV
+
+
+# ----------------------------------------------------------------------------- int8, 64-wide row blocks
+
+I8R64 = 3
+
+
+def test_i8_row64_dtype_and_scale_pointers():
+    assert call_step(md=I8R64, ms=0) == NULLP
+    assert call_step(md=I8R64, vs=BASE["vs"] + 4) == MISAL
+    assert call_step(md=4) == DTYPE
+    # the rule API takes fp32 / bf16 state only
+    assert call_opt("adamw", md=I8R64) == DTYPE
+
+
+@pytest.mark.skipif(_gpu_visible(), reason="on a GPU machine a valid call would launch on fake pointers")
+def test_i8_row64_scale_extent_is_the_row_layout():
+    """d_in 128, d_out 256: row-block scales are 256 x 2 fp32 (2 KiB), column-block ones
+    1 x 128 (512 B).  v_scale 1 KiB after m_scale overlaps only in the row layout."""
+    vs = BASE["ms"] + 1024
+    assert call_step(md=I8R64, vs=vs) == ALIAS
+    assert call_step(md=I8, vs=vs) == NODEV
+    assert call_step(md=I8R64) == NODEV
+    assert call_unfused(md=I8R64) == NODEV

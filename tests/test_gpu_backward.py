@@ -116,7 +116,7 @@ def _gpu_state(p):
     return st
 
 
-@pytest.mark.parametrize("moment", ["f32", "bf16", "i8"])
+@pytest.mark.parametrize("moment", ["f32", "bf16", "i8", "i8r64"])
 def test_backward_equals_input_grad_then_step_bitwise(moment):
     p = make_problem(300, 392, 520, moment, seed=41)
     T, d_in, d_out = p.shape
@@ -136,7 +136,7 @@ def test_backward_equals_input_grad_then_step_bitwise(moment):
     assert not torch.equal(a[2], dev(p.W))
 
 
-@pytest.mark.parametrize("moment", ["f32", "bf16", "i8"])
+@pytest.mark.parametrize("moment", ["f32", "bf16", "i8", "i8r64"])
 def test_backward_matches_oracle(moment):
     p = make_problem(256, 264, 328, moment, seed=42)
     T, d_in, d_out = p.shape
@@ -163,7 +163,7 @@ def _qkv(moment, T=200, d_in=264, outs=(264, 72, 72), seed=50):
     return mats
 
 
-@pytest.mark.parametrize("moment", ["bf16", "i8"])
+@pytest.mark.parametrize("moment", ["bf16", "i8", "i8r64"])
 def test_backward_grouped_sums_projections_of_one_input(moment):
     ps = _qkv(moment)
     T, d_in = ps[0].X.shape

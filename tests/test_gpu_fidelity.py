@@ -18,7 +18,8 @@ Arms (W is bf16 in all of them):
                 bf16 pipeline), fp32 or bf16 moments
 * decomposed    the two-kernel path with an fp32 gradient: the control that differs from
                 the fused arm only in where G lives, not in its value
-* int8          forge_linear_step with int8 block-absmax moments (256-row blocks)
+* int8          forge_linear_step with int8 block-absmax moments: 256-row column blocks
+                with sqrt(v) stored, and the paper's 64-wide row blocks with v stored
 
 The paper's claim checked here: the fused arm's rms weight error is below the standard
 arm's, because the standard arm rounds every gradient to bf16 before the moments read it
@@ -61,9 +62,10 @@ def test_fidelity_twenty_steps():
     W0 = synth.gaussian((V, H), 0.02, 879_999, device=dev)
 
     def state(dt):
-        if dt == "i8":
+        if dt in ("i8", "i8r64"):
             z8 = torch.zeros((V, H), dtype=torch.int8, device=dev)
-            zs = torch.zeros(((V + 255) // 256, H), dtype=torch.float32, device=dev)
+            shape = ((V + 255) // 256, H) if dt == "i8" else (V, (H + 63) // 64)
+            zs = torch.zeros(shape, dtype=torch.float32, device=dev)
             return [W0.clone(), z8, z8.clone(), zs, zs.clone()]
         t = torch.float32 if dt == "f32" else torch.bfloat16
         z = torch.zeros((V, H), dtype=t, device=dev)
@@ -76,6 +78,7 @@ def test_fidelity_twenty_steps():
         "standard_bf16G_bf16m": ("unfused", "bf16", torch.bfloat16),
         "decomposed_f32G_f32m": ("unfused", "f32", torch.float32),
         "fused_int8m": ("fused", "i8", None),
+        "fused_int8r64m": ("fused", "i8r64", None),
     }
     st = {k: state(v[1]) for k, v in arms.items()}
     ws = {torch.bfloat16: torch.empty((V, H), dtype=torch.bfloat16, device=dev),
@@ -85,13 +88,15 @@ def test_fidelity_twenty_steps():
     mr = np.zeros((V, H))
     vr = np.zeros((V, H))
     # same-storage references: bf16 W and the arm's moment storage, exact G
-    MK = {"f32": oracle.MOMENT_F32, "bf16": oracle.MOMENT_BF16, "i8": oracle.MOMENT_I8}
+    MK = {"f32": oracle.MOMENT_F32, "bf16": oracle.MOMENT_BF16, "i8": oracle.MOMENT_I8,
+          "i8r64": oracle.MOMENT_I8_ROW64}
     zeros = {"f32": lambda: np.zeros((V, H), np.float32), "bf16": lambda: np.zeros((V, H), np.uint16),
-             "i8": lambda: np.zeros((V, H), np.int8)}
+             "i8": lambda: np.zeros((V, H), np.int8), "i8r64": lambda: np.zeros((V, H), np.int8)}
+    sshape = {"i8": ((V + 255) // 256, H), "i8r64": (V, (H + 63) // 64)}
     ss = {dt: dict(W=bits(W0), m=zeros[dt](), v=zeros[dt](),
-                   ms=np.zeros(((V + 255) // 256, H), np.float32) if dt == "i8" else None,
-                   vs=np.zeros(((V + 255) // 256, H), np.float32) if dt == "i8" else None)
-          for dt in ("f32", "bf16", "i8")}
+                   ms=np.zeros(sshape[dt], np.float32) if dt in sshape else None,
+                   vs=np.zeros(sshape[dt], np.float32) if dt in sshape else None)
+          for dt in ("f32", "bf16", "i8", "i8r64")}
     for t in range(1, STEPS + 1):
         X, dY = _inputs(t, dev)
         for k, (path, _, gdt) in arms.items():

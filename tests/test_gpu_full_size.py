@@ -71,11 +71,11 @@ def test_sweep_sampled_rows_in_bench_configuration():
 # (T, d_in, d_out): X (then dY) with just under 2^31 elements, T ragged against the
 # 32-token chunk; chunk 1 holds one token row and its other rows lie past 2^32 bytes.
 D_MAX = 65075256          # 33 * D_MAX = 2147483448 < 2^31 - 1, and a multiple of 8
-MAX_SHAPES = [(33, D_MAX, 8, "bf16"), (33, D_MAX, 8, "i8"), (33, 8, D_MAX, "bf16")]
+MAX_SHAPES = [(33, D_MAX, 8, "bf16"), (33, D_MAX, 8, "i8"), (33, D_MAX, 8, "i8r64"), (33, 8, D_MAX, "bf16")]
 
 
 @pytest.mark.parametrize("T,d_in,d_out,moment", MAX_SHAPES,
-                         ids=["X-2^31-bf16", "X-2^31-i8", "dY-2^31-bf16"])
+                         ids=["X-2^31-bf16", "X-2^31-i8", "X-2^31-i8r64", "dY-2^31-bf16"])
 def test_maximum_operand_size(T, d_in, d_out, moment):
     _say(f"max size T={T} d_in={d_in} d_out={d_out} {moment}")
     device = torch.device("cuda:0")
@@ -86,13 +86,23 @@ def test_maximum_operand_size(T, d_in, d_out, moment):
     W = synth.gaussian((d_out, d_in), 0.02, base + 2, device=device)
     mat = synth.Matrix("max", d_out, d_in, base)
     wl = synth.WORKLOADS["o_proj"]
-    if moment == "i8":
-        m, v, ms, vs = synth.random_i8_state(mat, wl, device=device)
+    if moment in ("i8", "i8r64"):
+        m, v, ms, vs = synth.random_i8_state(mat, wl, device=device, layout="col256" if moment == "i8" else "row64")
     else:
         m, v = synth.warm_moments(mat, wl, device=device, dtype=torch.bfloat16)
         ms = vs = None
     rng = np.random.default_rng(33)
-    if d_in > d_out:
+    if moment == "i8r64":
+        # sample whole 64-column blocks (a block's scale depends on all of its columns); the
+        # last block holds the 56 columns of the ragged tail
+        nb = (d_in + 63) // 64
+        blocks = _sample(nb, rng, 8, tile=2)
+        cols = torch.from_numpy(np.concatenate([np.arange(64 * b, min(64 * b + 64, d_in)) for b in blocks])).to(device)
+        bsel = torch.from_numpy(blocks).to(device)
+        sel = lambda t: t.index_select(1, cols)
+        p = Problem(bits(sel(X)), bits(dY), bits(sel(W)), bits(sel(m)), bits(sel(v)), moment,
+                    bits(ms.index_select(1, bsel)), bits(vs.index_select(1, bsel)), hp=dict(hp))
+    elif d_in > d_out:
         # sample columns: X[:, cols], W/m/v[:, cols] (int8 scales are per column as well)
         cols = torch.from_numpy(_sample(d_in, rng, 64)).to(device)
         sel = lambda t: t.index_select(1, cols)
@@ -108,7 +118,9 @@ def test_maximum_operand_size(T, d_in, d_out, moment):
     forge.forge_linear_step(X, dY, W, m, v, ms, vs, step=100, **hp)
     torch.cuda.synchronize()
     gpu = dict(W=bits(sel(W)), m=bits(sel(m)), v=bits(sel(v)))
-    if ms is not None:
+    if moment == "i8r64":
+        gpu.update(m_scale=bits(ms.index_select(1, bsel)), v_scale=bits(vs.index_select(1, bsel)))
+    elif ms is not None:
         gpu.update(m_scale=bits(sel(ms)), v_scale=bits(sel(vs)))
     _say(check_step(gpu, ora, moment, hp=p.hp))
 

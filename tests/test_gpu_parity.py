@@ -32,7 +32,7 @@ SMALL = [
 ]
 
 
-@pytest.mark.parametrize("moment", ["f32", "bf16", "i8"])
+@pytest.mark.parametrize("moment", ["f32", "bf16", "i8", "i8r64"])
 @pytest.mark.parametrize("shape", SMALL, ids=lambda s: "x".join(map(str, s)))
 def test_fused_matches_oracle(moment, shape):
     T, d_in, d_out = shape
@@ -117,7 +117,7 @@ def test_mlp_int8_full(idx):
     _full_matrix("mlp_i8", idx)
 
 
-@pytest.mark.parametrize("moment", ["f32", "bf16", "i8"])
+@pytest.mark.parametrize("moment", ["f32", "bf16", "i8", "i8r64"])
 def test_unfused_fp32_gradient_matches_oracle(moment):
     p = make_problem(96, 392, 264, moment, seed=17)
     ora = run_oracle(p, 9)
@@ -139,7 +139,7 @@ def _near_bf16_midpoint(G64, bound):
     return np.abs(np.abs(G64) - mid) <= bound
 
 
-@pytest.mark.parametrize("moment", ["bf16", "i8"])
+@pytest.mark.parametrize("moment", ["bf16", "i8", "i8r64"])
 def test_unfused_bf16_gradient_matches_rounded_oracle(moment):
     """The two-kernel path with a bf16 gradient buffer equals the oracle that rounds G to
     bf16 first (App. B truncation), except where G sits on a bf16 rounding midpoint."""
@@ -150,7 +150,7 @@ def test_unfused_bf16_gradient_matches_rounded_oracle(moment):
     _say(f"near-midpoint gradients exempted: {int(exempt.sum())} of {exempt.size}")
     # the worst-case bound is loose (T 2^-24 sum|terms|), so a few percent sit in its window
     assert exempt.mean() < 0.10
-    if moment == "i8":
+    if moment in ("i8", "i8r64"):
         # a flipped gradient rounding moves a whole block's codes at most by a tie; check W only
         keep = ~exempt
         ulps = np.abs(bf16_key(gpu["W"]) - bf16_key(ora["W"]))[keep]
@@ -206,7 +206,7 @@ def _state_on_gpu(p):
     return st + sc
 
 
-@pytest.mark.parametrize("moment", ["f32", "bf16", "i8"])
+@pytest.mark.parametrize("moment", ["f32", "bf16", "i8", "i8r64"])
 def test_grouped_matches_oracle_and_single_calls(moment):
     """forge_linear_step_grouped: every matrix as the oracle has it, and bit-identical to
     a separate forge_linear_step call on that matrix (Def. 1: tiles are independent)."""
@@ -226,7 +226,7 @@ def test_grouped_matches_oracle_and_single_calls(moment):
     torch.cuda.synchronize()
     for p, g, s1 in zip(probs, group, single):
         out = dict(W=bits(g[2]), m=bits(g[3]), v=bits(g[4]))
-        if moment == "i8":
+        if moment in ("i8", "i8r64"):
             out.update(m_scale=bits(g[5]), v_scale=bits(g[6]))
         _say(check_step(out, run_oracle(p, 100), moment, hp=p.hp))
         for a, b in zip(g[2:], s1):

@@ -638,3 +638,89 @@ def test_unrounded_adamw_reference_equals_the_oracle_before_rounding():
         np.testing.assert_allclose(W1, ora["W64"], rtol=1e-15, atol=0)
         np.testing.assert_allclose(m1, ora["m64"], rtol=1e-15, atol=0)
         np.testing.assert_allclose(v1, ora["v64"], rtol=1e-15, atol=0)
+
+
+# ------------------------------------------------------------------------- int8, 64-wide row blocks
+
+from oracle import MOMENT_I8_ROW64  # noqa: E402
+
+
+def test_i8_row64_quantizer_invariants():
+    """App. B's layout: one scale per 64 consecutive elements of a row (a ragged last block
+    when d_in is not a multiple of 64), s = absmax/127, |code| <= 127 with the absmax at
+    +-127, and every element within half a step of its code."""
+    rng = np.random.default_rng(11)
+    d_out, d_in = 5, 200                    # blocks of 64, 64, 64, 8 per row
+    x = rng.standard_normal((d_out, d_in)) * 10.0 ** rng.integers(-6, 0, (d_out, 1))
+    x[2, 64:128] = 0.0                      # an all-zero block
+    codes, scales = oracle.quantize_i8_row64(x, second_moment=False)
+    assert scales.shape == (d_out, 4)
+    for p in range(d_out):
+        for b in range(4):
+            blk = slice(64 * b, min(64 * b + 64, d_in))
+            a = np.float32(np.abs(x[p, blk].astype(np.float32)).max())
+            assert scales[p, b] == np.float32(a / np.float32(127.0))
+            if a > 0:
+                assert np.abs(codes[p, blk]).max() == 127
+                err = np.abs(scales[p, b] * codes[p, blk].astype(np.float64) - x[p, blk])
+                assert np.all(err <= 0.5 * scales[p, b] * (1 + 1e-6) + 1e-7 * np.abs(x[p, blk]))
+            else:
+                assert not codes[p, blk].any()
+    # a change in one element moves only its own block's scale
+    y = x.copy()
+    y[1, 70] *= 100.0
+    _, s2 = oracle.quantize_i8_row64(y, second_moment=False)
+    changed = np.argwhere(s2 != scales)
+    assert changed.tolist() == [[1, 1]]
+
+
+def test_i8_row64_second_moment_floor_and_no_square_root():
+    v = np.abs(np.random.default_rng(12).standard_normal((3, 128))) * 1e-6
+    v[0, :64] = 0.0
+    v[1, 5] = 1e-20                          # tiny next to its block's max
+    codes, scales = oracle.quantize_i8_row64(v, second_moment=True)
+    assert not codes[0, :64].any() and scales[0, 0] == 0.0
+    assert codes[1, 5] == 1                  # floored away from zero
+    assert np.all(codes[np.repeat(scales, 64, axis=1) > 0] >= 1)
+    # v itself is stored: the block max maps to 127 and decodes to v (no sqrt)
+    np.testing.assert_allclose(oracle.dequantize_i8_row64(codes, scales).max(axis=1)[1:],
+                               v.max(axis=1)[1:], rtol=1e-6)
+
+
+def test_i8_row64_first_moment_accumulated_error_bound():
+    """App. B: re-quantising every step keeps |m_q - m| <= s/(2(1-b1)), s the largest scale
+    the block has had."""
+    rng = np.random.default_rng(13)
+    d_out, d_in, b1 = 4, 192, 0.9
+    W = bf16_rand((d_out, d_in), 0.02, 48)
+    m_exact = np.zeros((d_out, d_in))
+    mq, ms = oracle.quantize_i8_row64(m_exact, second_moment=False)
+    vq, vs = oracle.quantize_i8_row64(np.full((d_out, d_in), 1e-6), second_moment=True)
+    smax = np.zeros_like(ms)
+    for t in range(1, 41):
+        G = rng.standard_normal((d_out, d_in)) * 0.02
+        out = oracle.adamw(G, W, mq, vq, m_scale=ms, v_scale=vs, moment_dtype=MOMENT_I8_ROW64, step=t,
+                           **dict(HP, beta1=b1))
+        m_exact = f32(b1) * m_exact + (1 - f32(b1)) * G
+        mq, vq, ms, vs = out["m"], out["v"], out["m_scale"], out["v_scale"]
+        smax = np.maximum(smax, ms)
+        err = np.abs(oracle.dequantize_i8_row64(mq, ms) - m_exact)
+        assert np.all(err <= np.repeat(smax, 64, axis=1) / (2 * (1 - f32(b1))) * (1 + 1e-4))
+
+
+def test_i8_row64_step_reads_unquantized_state_for_the_weight():
+    rng = np.random.default_rng(14)
+    d_out, d_in = 6, 136
+    G = rng.standard_normal((d_out, d_in)) * 0.02
+    W = bf16_rand((d_out, d_in), 0.02, 49)
+    mq, ms = oracle.quantize_i8_row64(rng.standard_normal((d_out, d_in)) * 1e-3, second_moment=False)
+    vq, vs = oracle.quantize_i8_row64(np.abs(rng.standard_normal((d_out, d_in))) * 1e-6, second_moment=True)
+    out = oracle.adamw(G, W, mq, vq, m_scale=ms, v_scale=vs, moment_dtype=MOMENT_I8_ROW64, step=5, **HP)
+    W1, m1, v1 = oracle.adamw_f64(G, oracle.bf16_bits_to_f64(W), oracle.dequantize_i8_row64(mq, ms),
+                                  oracle.dequantize_i8_row64(vq, vs), step=5, **HP)
+    np.testing.assert_allclose(out["W64"], W1, rtol=1e-15)
+    np.testing.assert_allclose(out["m64"], m1, rtol=1e-15)
+    np.testing.assert_allclose(out["v64"], v1, rtol=1e-15)
+    # and the stored state is that unquantised state, re-quantised
+    qm, sm = oracle.quantize_i8_row64(m1, second_moment=False)
+    assert np.array_equal(qm, out["m"]) and np.array_equal(sm, out["m_scale"])
