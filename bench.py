@@ -56,8 +56,9 @@ def build_workload(wl, device, moment_override=None):
     for mat in wl.matrices:
         X, dY = synth.activations(wl.T, mat, wl, wl.steps[0], device=device)
         W = synth.weight(mat, wl, device=device)
-        if wl.moment == "i8":
-            mq, vq, ms, vs = synth.random_i8_state(mat, wl, device=device)
+        if wl.moment in ("i8", "i8r64"):
+            mq, vq, ms, vs = synth.random_i8_state(mat, wl, device=device,
+                                                   layout="col256" if wl.moment == "i8" else "row64")
             mats.append(dict(mat=mat, X=X, dY=dY, W=W, m=mq, v=vq, ms=ms, vs=vs))
         else:
             dt = torch.bfloat16 if wl.moment == "bf16" else torch.float32
@@ -170,7 +171,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="sweep", choices=["sweep", "o_proj", "mlp", "mlp_i8"])
+    ap.add_argument("--workload", default="sweep", choices=["sweep", "o_proj", "mlp", "mlp_i8", "mlp_i8r64"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
     ap.add_argument("--tokens", type=int, default=None,
@@ -252,7 +253,8 @@ def main():
             "workload": {"sweep": "Llama-3.1-8B linear-layer sweep: 32 x {q,k,v,o,gate,up,down} + lm_head, T=512, bf16 W/m/v",
                          "o_proj": "Llama-3.1-8B o_proj 4096x4096, T=512, bf16 W/m/v",
                          "mlp": "Llama-3.1-8B gate/up/down, T=512, bf16 W/m/v",
-                         "mlp_i8": "Llama-3.1-8B gate/up/down, T=512, int8 m/v"}[args.workload]
+                         "mlp_i8": "Llama-3.1-8B gate/up/down, T=512, int8 m/v (256-row blocks)",
+                         "mlp_i8r64": "Llama-3.1-8B gate/up/down, T=512, int8 m/v (64-wide row blocks)"}[args.workload]
                         .replace("T=512", f"T={T}"),
             "T": T, "matrices": len(mats),
             "params": sum(d["mat"].d_in * d["mat"].d_out for d in mats),

@@ -60,13 +60,27 @@ typedef enum {
                               block scheme follows App. B (re-quantised every step, second
                               moment kept away from zero: its codes are at least 1 in any
                               non-zero block). */
-    FORGE_MOMENT_I8_ROW64 = 3 /* the paper's own int8 layout (App. B): one fp32 absmax scale
+    FORGE_MOMENT_I8_ROW64 = 3, /* the paper's own int8 layout (App. B): one fp32 absmax scale
                               per 64 consecutive elements of a row (along d_in, a shorter last
                               block when d_in is not a multiple of 64): m = s_m * q_m and
                               v = s_v * q_v (v itself stored); scales are
                               [d_out, ceil(d_in/64)] fp32; same rounding and v floor as above.
                               forge_linear_step(_grouped), the backward calls and forge_adamw
                               accept it; forge_linear_step_opt does not. */
+    FORGE_MOMENT_FP8 = 4   /* fp8 (OCP E4M3, largest finite 448, round to nearest even, values
+                              clamped into range) codes of m and of sqrt(v), each tensor with
+                              one delayed scale s = amax / 448: m = s_m * e4m3(q_m),
+                              v = (s_v * e4m3(q_v))^2, and a sqrt(v) > 0 never stored as zero.
+                              m_scale and v_scale each point to a ring of 4 fp32 amax slots
+                              (16 bytes, caller-owned, all zero for a cold start with zero
+                              codes).  Step t decodes with the scale of slot (t-2)%4, encodes
+                              with slot (t-1)%4 (a scale of 1 while a slot is 0), records the
+                              max |m'| and max sqrt(v') of its own values into slot t%4 and
+                              clears slot (t+1)%4: consecutive calls on a tensor must pass
+                              consecutive steps.  App. E's per-tensor delayed-scaled fp8 mode.
+                              forge_linear_step(_grouped), the backward calls and
+                              forge_linear_step_wfp8 accept it; forge_adamw and
+                              forge_linear_step_unfused do not. */
 } forge_moment_dtype;
 
 /* Element type of a materialised gradient (only the two-kernel path stores one). */
@@ -225,6 +239,25 @@ FORGE_API forge_status forge_linear_step_opt(const void *X, const void *dY, void
                                              int64_t T, int64_t d_in, int64_t d_out, int32_t optimizer,
                                              int32_t state_dtype, const forge_hparams *hp, int64_t step,
                                              void *stream);
+
+/*
+ * forge_linear_step_wfp8 -- forge_linear_step with the weight stored in fp8: W holds OCP
+ * E4M3 codes [d_out, d_in] (1 byte each) with a per-tensor delayed scale kept in the 4-slot
+ * amax ring `w_amax` (the scheme of FORGE_MOMENT_FP8, applied to max |W'|).  The epilogue
+ * decodes W, steps it in fp32 and encodes it again, so that weight quantisation costs no
+ * pass of its own (Sec. 3, the FP8 weight and weight+moment recipes).
+ *
+ *   moment_dtype   FORGE_MOMENT_BF16 (m_amax, v_amax ignored) or FORGE_MOMENT_FP8
+ *   other arguments as in forge_linear_step
+ *
+ * Errors as in forge_linear_step; FORGE_ERR_INVALID_DTYPE for another moment dtype; NULL
+ * w_amax: FORGE_ERR_NULL_POINTER.
+ */
+FORGE_API forge_status forge_linear_step_wfp8(const void *X, const void *dY, void *W, float *w_amax, void *m,
+                                              void *v, float *m_amax, float *v_amax, int64_t T, int64_t d_in,
+                                              int64_t d_out, int32_t moment_dtype, float lr, float beta1,
+                                              float beta2, float eps, float weight_decay, int64_t step,
+                                              void *stream);
 
 /*
  * forge_input_grad -- the layer's input gradient dX = dY W (Algorithm 1, first line; the

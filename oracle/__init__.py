@@ -67,6 +67,13 @@ def _load():
             lib.forge_oracle_adamw_i8row.argtypes = [P, P, P, P, P, P, I64, I64, F32, F32, F32, F32, F32, I64,
                                                      P, P, P, P, P]
             lib.forge_oracle_adamw_i8row.restype = None
+            lib.forge_oracle_e4m3_decode.argtypes = [ctypes.c_uint8]
+            lib.forge_oracle_e4m3_decode.restype = ctypes.c_double
+            lib.forge_oracle_e4m3_encode_array.argtypes = [P, I64, P]
+            lib.forge_oracle_e4m3_encode_array.restype = None
+            lib.forge_oracle_adamw_fp8.argtypes = [P, P, I32, P, P, P, I32, P, P, I64, I64, F32, F32, F32, F32, F32,
+                                                   I64, P, P, P, P, P, P]
+            lib.forge_oracle_adamw_fp8.restype = None
             lib.forge_oracle_input_grad.argtypes = [P, P, I64, I64, I64, P]
             lib.forge_oracle_input_grad.restype = None
             lib.forge_oracle_quantize_i8.argtypes = [P, I64, I64, I32, P, P]
@@ -276,6 +283,45 @@ def _adamw_i8row(G, W, m, v, m_scale, v_scale, *, lr, beta1, beta2, eps, weight_
     if qm is not None:
         out.update(qm=qm, qv=qv)
     return out
+
+
+def e4m3_decode(codes: np.ndarray) -> np.ndarray:
+    """E4M3 (OCP) codes -> fp64 values."""
+    lib = _load()
+    c = np.ascontiguousarray(codes, dtype=np.uint8)
+    return np.array([lib.forge_oracle_e4m3_decode(int(x)) for x in c.reshape(-1)]).reshape(c.shape)
+
+
+def e4m3_encode(x) -> np.ndarray:
+    """fp32 values within [-448, 448] -> nearest E4M3 codes, ties to even."""
+    x = np.ascontiguousarray(np.asarray(x, dtype=np.float32))
+    out = np.empty(x.shape, dtype=np.uint8)
+    _load().forge_oracle_e4m3_encode_array(_ptr(x), x.size, _ptr(out))
+    return out
+
+
+def adamw_fp8(G, W, m, v, *, w_fp8, m_fp8, w_ring=None, m_ring=None, v_ring=None, lr, beta1, beta2, eps,
+              weight_decay, step):
+    """One AdamW step with fp8 (E4M3, per-tensor delayed scale) weights and / or moments.
+
+    W: E4M3 codes (uint8) when ``w_fp8``, else bf16 bits; m, v: E4M3 codes of m and sqrt(v)
+    when ``m_fp8``, else bf16 bits; rings: fp32 [4] amax slots.  Inputs are not modified.
+    Returns the new W, m, v, rings, the fp64 W64, m64, v64 and the encoded fp32 quotients
+    qw, qm, qv.
+    """
+    G = _c(G, np.float64)
+    d_out, d_in = G.shape
+    W = _c(W, np.uint8 if w_fp8 else np.uint16).copy()
+    m = _c(m, np.uint8 if m_fp8 else np.uint16).copy()
+    v = _c(v, np.uint8 if m_fp8 else np.uint16).copy()
+    rings = [_c(r, np.float32).copy() if r is not None else None for r in (w_ring, m_ring, v_ring)]
+    W64, m64, v64, qw, qm, qv = (np.empty((d_out, d_in), dtype=np.float64) for _ in range(6))
+    _load().forge_oracle_adamw_fp8(_ptr(G), _ptr(W), int(bool(w_fp8)), _ptr(rings[0]), _ptr(m), _ptr(v),
+                                   int(bool(m_fp8)), _ptr(rings[1]), _ptr(rings[2]), d_in, d_out, float(lr),
+                                   float(beta1), float(beta2), float(eps), float(weight_decay), int(step),
+                                   _ptr(W64), _ptr(m64), _ptr(v64), _ptr(qw), _ptr(qm), _ptr(qv))
+    return dict(W=W, m=m, v=v, w_ring=rings[0], m_ring=rings[1], v_ring=rings[2], W64=W64, m64=m64, v64=v64,
+                qw=qw, qm=qm, qv=qv)
 
 
 def linear_step(X, dY, W, m, v, **kw):

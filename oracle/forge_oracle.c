@@ -34,6 +34,15 @@
  * code = round_half_even(x/s) clamped to [-127, 127], for m and for v itself (no square
  * root), the v codes floored at 1 inside non-zero blocks; decision in fp32 as above.
  *
+ * fp8 encodings (forge_oracle_adamw_fp8; App. E's per-tensor delayed-scaled fp8 states and
+ * the fp8-weight recipe of Sec. 3): OCP E4M3 codes (1 sign, 4 exponent bits with bias 7,
+ * 3 mantissa bits, largest finite 448, subnormals below 2^-6), encoded round-half-even from
+ * the fp32 quotient x/s clamped to [-448, 448]; one scale per tensor, s = amax/448 from a
+ * previous step's amax (1 while there is none), kept in a ring of 4 amax slots: step t
+ * decodes with slot (t-2)%4, encodes with slot (t-1)%4, max-reduces the fp32 magnitudes of
+ * its new values (|W'|, |m'|, sqrt(v')) into slot t%4 and clears slot (t+1)%4.  sqrt(v) is
+ * what is stored for the second moment, and a positive one never encodes to zero.
+ *
  * Other update rules (forge_oracle_rule_step): the coordinate-wise optimizer families of
  * the paper's family table (App. I) and Muon's momentum accumulate (regime 2 of App. A).
  * The paper states that each was checked against its reference implementation and does
@@ -394,6 +403,124 @@ void forge_oracle_adamw_i8row(const double *G, uint16_t *W, int8_t *m, int8_t *v
     forge_oracle_quantize_i8_row64(vn, d_in, d_out, 1, v, v_scale, qv);
     free(mn);
     free(vn);
+}
+
+/* ------------------------------------------------------------- fp8 (E4M3) encodings */
+
+/* E4M3 code -> value (the OCP definition; codes 0x7F and 0xFF are NaN). */
+double forge_oracle_e4m3_decode(uint8_t c)
+{
+    const int sign = c >> 7, e = (c >> 3) & 0xF, m = c & 7;
+    if (e == 15 && m == 7) return NAN;
+    const double v = e == 0 ? ldexp((double)m / 8.0, -6) : ldexp(1.0 + (double)m / 8.0, e - 7);
+    return sign ? -v : v;
+}
+
+/* fp32 value, already within [-448, 448] -> nearest E4M3 code, ties to even. */
+uint8_t forge_oracle_e4m3_encode(float x)
+{
+    const uint8_t sign = signbit(x) ? 0x80 : 0;
+    double a = fabs((double)x);
+    if (a > 448.0) a = 448.0;
+    if (a < ldexp(1.0, -6)) {                   /* subnormal range: steps of 2^-9 */
+        const double q = rint(ldexp(a, 9));      /* 0..8; 8 is the smallest normal, code 8 */
+        return (uint8_t)(sign | (uint8_t)q);
+    }
+    int e;
+    (void)frexp(a, &e);                          /* a = f * 2^e, 0.5 <= f < 1: exponent e - 1 */
+    e -= 1;
+    double q = rint(ldexp(a, 3 - e));            /* 8..16: the significand with 3 fraction bits */
+    if (q == 16.0) {
+        q = 8.0;
+        e += 1;
+    }
+    return (uint8_t)(sign | (uint8_t)(((e + 7) << 3) | ((int)q - 8)));
+}
+
+void forge_oracle_e4m3_encode_array(const float *x, int64_t n, uint8_t *out)
+{
+    for (int64_t i = 0; i < n; ++i) out[i] = forge_oracle_e4m3_encode(x[i]);
+}
+
+static float fp8_scale_of(float amax) { return amax > 0.0f ? amax / 448.0f : 1.0f; }
+
+static float clamp448(float x) { return x > 448.0f ? 448.0f : (x < -448.0f ? -448.0f : x); }
+
+/*
+ * One AdamW step (Algorithm 1, fp64) with fp8 tensors.  w_fp8: W holds E4M3 codes with ring
+ * w_ring, else bf16 bits.  m_fp8: m, v hold E4M3 codes of m and sqrt(v) with rings m_ring,
+ * v_ring, else bf16 bits.  W64, m64, v64 (optional): unrounded fp64 results; qw, qm, qv
+ * (optional): the fp32 quotients x/s that were encoded (0 where a tensor is bf16).
+ */
+void forge_oracle_adamw_fp8(const double *G, void *W, int w_fp8, float *w_ring, void *m, void *v, int m_fp8,
+                            float *m_ring, float *v_ring, int64_t d_in, int64_t d_out, float lr, float beta1,
+                            float beta2, float eps, float weight_decay, int64_t step, double *W64, double *m64,
+                            double *v64, double *qw, double *qm, double *qv)
+{
+    const double b1 = beta1, b2 = beta2, eta = lr, lam = weight_decay, ep = eps;
+    const double bc1 = 1.0 - pow(b1, (double)step), bc2 = 1.0 - pow(b2, (double)step);
+    const double wdf = 1.0 - eta * lam;
+    const int slot = (int)(step % 4), enc = (slot + 3) % 4, dec = (slot + 2) % 4, clr = (slot + 1) % 4;
+    const float w_dec = w_fp8 ? fp8_scale_of(w_ring[dec]) : 1.0f, w_enc = w_fp8 ? fp8_scale_of(w_ring[enc]) : 1.0f;
+    const float m_dec = m_fp8 ? fp8_scale_of(m_ring[dec]) : 1.0f, m_enc = m_fp8 ? fp8_scale_of(m_ring[enc]) : 1.0f;
+    const float v_dec = m_fp8 ? fp8_scale_of(v_ring[dec]) : 1.0f, v_enc = m_fp8 ? fp8_scale_of(v_ring[enc]) : 1.0f;
+    float aw = 0.0f, am = 0.0f, av = 0.0f;
+    for (int64_t k = 0; k < d_in * d_out; ++k) {
+        double w0, m0, v0;
+        if (w_fp8) w0 = (double)w_dec * forge_oracle_e4m3_decode(((uint8_t *)W)[k]);
+        else w0 = forge_oracle_bf16_to_f64(((uint16_t *)W)[k]);
+        if (m_fp8) {
+            m0 = (double)m_dec * forge_oracle_e4m3_decode(((uint8_t *)m)[k]);
+            const double r0 = (double)v_dec * forge_oracle_e4m3_decode(((uint8_t *)v)[k]);
+            v0 = r0 * r0;
+        } else {
+            m0 = forge_oracle_bf16_to_f64(((uint16_t *)m)[k]);
+            v0 = forge_oracle_bf16_to_f64(((uint16_t *)v)[k]);
+        }
+        const double g = G[k];
+        const double m1 = b1 * m0 + (1.0 - b1) * g;
+        const double v1 = b2 * v0 + (1.0 - b2) * g * g;
+        const double w1 = wdf * w0 - eta * (m1 / bc1) / (sqrt(v1 / bc2) + ep);
+        const double r1 = sqrt(v1);
+        if (W64) W64[k] = w1;
+        if (m64) m64[k] = m1;
+        if (v64) v64[k] = v1;
+        if (w_fp8) {
+            const float qf = (float)w1 / w_enc;
+            ((uint8_t *)W)[k] = forge_oracle_e4m3_encode(clamp448(qf));
+            if (qw) qw[k] = qf;
+            if (fabsf((float)w1) > aw) aw = fabsf((float)w1);
+        } else {
+            ((uint16_t *)W)[k] = forge_oracle_f64_to_bf16(w1);
+            if (qw) qw[k] = 0.0;
+        }
+        if (m_fp8) {
+            const float qmf = (float)m1 / m_enc, qvf = (float)r1 / v_enc;
+            uint8_t cv = forge_oracle_e4m3_encode(clamp448(qvf));
+            if (r1 > 0.0 && (cv & 0x7F) == 0) cv = 1;
+            ((uint8_t *)m)[k] = forge_oracle_e4m3_encode(clamp448(qmf));
+            ((uint8_t *)v)[k] = cv;
+            if (qm) qm[k] = qmf;
+            if (qv) qv[k] = qvf;
+            if (fabsf((float)m1) > am) am = fabsf((float)m1);
+            if ((float)r1 > av) av = (float)r1;
+        } else {
+            ((uint16_t *)m)[k] = forge_oracle_f64_to_bf16(m1);
+            ((uint16_t *)v)[k] = forge_oracle_f64_to_bf16(v1);
+            if (qm) qm[k] = 0.0;
+            if (qv) qv[k] = 0.0;
+        }
+    }
+    if (w_fp8) {
+        if (aw > w_ring[slot]) w_ring[slot] = aw;
+        w_ring[clr] = 0.0f;
+    }
+    if (m_fp8) {
+        if (am > m_ring[slot]) m_ring[slot] = am;
+        if (av > v_ring[slot]) v_ring[slot] = av;
+        m_ring[clr] = 0.0f;
+        v_ring[clr] = 0.0f;
+    }
 }
 
 /* ------------------------------------------------------------- other update rules */

@@ -6,9 +6,10 @@ weight-gradient GEMM reads X and dY once and costs 2*T flops per parameter.
 """
 from __future__ import annotations
 
-MOMENT_BYTES = {"f32": 4, "bf16": 2, "i8": 1}
+MOMENT_BYTES = {"f32": 4, "bf16": 2, "i8": 1, "i8r64": 1}
 GRAD_BYTES = {"bf16": 2, "f32": 4}
-I8_BLOCK = 256
+I8_BLOCK = 256          # rows of d_out per scale, 256-row column layout
+I8_ROW_BLOCK = 64       # elements of a row per scale, 64-wide row layout
 
 
 def state_bytes_per_param(moment: str) -> float:
@@ -22,6 +23,8 @@ def fused_bytes(T: int, d_in: int, d_out: int, moment: str) -> int:
     if moment == "i8":
         nblk = (d_out + I8_BLOCK - 1) // I8_BLOCK
         b += 2 * 2 * 4 * nblk * d_in          # two fp32 scale tensors, read and written
+    elif moment == "i8r64":
+        b += 2 * 2 * 4 * d_out * ((d_in + I8_ROW_BLOCK - 1) // I8_ROW_BLOCK)
     return int(b)
 
 

@@ -32,12 +32,17 @@ bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 int64_t moment_bytes(int32_t md) { return md == FORGE_MOMENT_F32 ? 4 : md == FORGE_MOMENT_BF16 ? 2 : 1; }
 
-bool is_int8(int32_t md) { return md == FORGE_MOMENT_I8 || md == FORGE_MOMENT_I8_ROW64; }
+// Moment dtypes with scale tensors (int8 block scales, fp8 amax rings).
+bool is_int8(int32_t md)
+{
+    return md == FORGE_MOMENT_I8 || md == FORGE_MOMENT_I8_ROW64 || md == FORGE_MOMENT_FP8;
+}
 
 // Bytes of one int8 scale tensor of a [d_out, d_in] moment.
 int64_t scale_bytes(int32_t md, int64_t d_in, int64_t d_out)
 {
     if (md == FORGE_MOMENT_I8_ROW64) return d_out * ((d_in + 63) / 64) * 4;
+    if (md == FORGE_MOMENT_FP8) return 4 * forge_impl::AMAX_SLOTS;
     return ((d_out + 255) / 256) * d_in * 4;
 }
 
@@ -46,7 +51,7 @@ bool finite(float x) { return std::isfinite(x); }
 forge_status check_dtype_moment(int32_t md)
 {
     return (md == FORGE_MOMENT_F32 || md == FORGE_MOMENT_BF16 || md == FORGE_MOMENT_I8 ||
-            md == FORGE_MOMENT_I8_ROW64)
+            md == FORGE_MOMENT_I8_ROW64 || md == FORGE_MOMENT_FP8)
                ? FORGE_OK : FORGE_ERR_INVALID_DTYPE;
 }
 
@@ -97,9 +102,15 @@ Hyper make_hyper(float lr, float b1, float b2, float eps, float wd, int64_t step
 }
 
 // The optimizer-state tensors of one step: pointers, alignment and mutual disjointness.
+// At most W, m, v, two scale tensors (or amax rings) and the weight's amax ring.
 struct StateSet {
-    Range r[5];
+    static constexpr int CAP = 8;
+    Range r[CAP];
     int n = 0;
+    void add(Range x)
+    {
+        if (n < CAP) r[n++] = x;
+    }
 };
 
 forge_status check_state(void *W, void *m, void *v, float *ms, float *vs, int64_t d_in,
@@ -237,6 +248,7 @@ forge_status plan_group(const forge_matrix *mats, int32_t n, int64_t T, int32_t 
         a.ms = x.m_scale;
         a.vs = x.v_scale;
         a.h = h;
+        a.slot = static_cast<int>(step % forge_impl::AMAX_SLOTS);
     }
     return FORGE_OK;
 }
@@ -405,6 +417,7 @@ forge_status forge_linear_step(const void *X, const void *dY, void *W, void *m, 
     a.ms = m_scale;
     a.vs = v_scale;
     a.h = make_hyper(lr, beta1, beta2, eps, weight_decay, step);
+    a.slot = static_cast<int>(step % forge_impl::AMAX_SLOTS);
     return from_hip(forge_impl::launch_fused(a, md, static_cast<hipStream_t>(stream)));
 }
 
@@ -423,6 +436,55 @@ forge_status forge_linear_step_grouped(const forge_matrix *mats, int32_t n, int6
     if (g.nlive == 0) return FORGE_OK;
     if ((s = check_device()) != FORGE_OK) return s;
     return from_hip(forge_impl::launch_fused_group(g.args, g.nlive, md, static_cast<hipStream_t>(stream)));
+}
+
+forge_status forge_linear_step_wfp8(const void *X, const void *dY, void *W, float *w_amax, void *m, void *v,
+                                    float *m_amax, float *v_amax, int64_t T, int64_t d_in, int64_t d_out,
+                                    int32_t md, float lr, float beta1, float beta2, float eps,
+                                    float weight_decay, int64_t step, void *stream)
+{
+    forge_status s;
+    bool empty = false;
+    if (md != FORGE_MOMENT_BF16 && md != FORGE_MOMENT_FP8) return FORGE_ERR_INVALID_DTYPE;
+    if ((s = check_shape(T, d_in, d_out, empty)) != FORGE_OK) return s;
+    if (empty) return FORGE_OK;
+    if ((s = check_inputs(X, dY, T, d_in, d_out)) != FORGE_OK) return s;
+    const bool f8 = (md == FORGE_MOMENT_FP8);
+    if (!W || !w_amax || !m || !v || (f8 && (!m_amax || !v_amax))) return FORGE_ERR_NULL_POINTER;
+    if (!aligned16(W) || !aligned16(w_amax) || !aligned16(m) || !aligned16(v) ||
+        (f8 && (!aligned16(m_amax) || !aligned16(v_amax))))
+        return FORGE_ERR_MISALIGNED;
+    const int64_t P = d_in * d_out, ring = 4 * forge_impl::AMAX_SLOTS;
+    StateSet st;
+    st.add(range_of(W, P));
+    st.add(range_of(m, moment_bytes(md) * P));
+    st.add(range_of(v, moment_bytes(md) * P));
+    if (f8) {
+        st.add(range_of(m_amax, ring));
+        st.add(range_of(v_amax, ring));
+    }
+    const Range rw = range_of(w_amax, ring);
+    for (int i = 0; i < st.n; ++i) {
+        if (overlap(st.r[i], rw)) return FORGE_ERR_ALIASING;
+        for (int j = i + 1; j < st.n; ++j)
+            if (overlap(st.r[i], st.r[j])) return FORGE_ERR_ALIASING;
+    }
+    st.add(rw);
+    if ((s = check_hyper(lr, beta1, beta2, eps, weight_decay, step)) != FORGE_OK) return s;
+    if (T > 0 && (!disjoint_from(st, range_of(X, 2 * T * d_in)) || !disjoint_from(st, range_of(dY, 2 * T * d_out))))
+        return FORGE_ERR_ALIASING;
+    if ((s = check_device()) != FORGE_OK) return s;
+
+    Args a = base_args(X, dY, T, d_in, d_out);
+    a.W = static_cast<uint16_t *>(W);          // fp8 codes; the kernel reads it as bytes
+    a.wr = w_amax;
+    a.m = m;
+    a.v = v;
+    a.ms = f8 ? m_amax : nullptr;
+    a.vs = f8 ? v_amax : nullptr;
+    a.h = make_hyper(lr, beta1, beta2, eps, weight_decay, step);
+    a.slot = static_cast<int>(step % forge_impl::AMAX_SLOTS);
+    return from_hip(forge_impl::launch_fused_wfp8(&a, 1, md, static_cast<hipStream_t>(stream)));
 }
 
 forge_status forge_input_grad(const void *dY, const void *W, void *dX, int64_t T, int64_t d_in,
@@ -521,7 +583,7 @@ forge_status forge_linear_step_opt(const void *X, const void *dY, void *W, void 
         if (!need[k]) continue;
         if (!t[k]) return FORGE_ERR_NULL_POINTER;
         if (!aligned16(t[k])) return FORGE_ERR_MISALIGNED;
-        st.r[st.n++] = range_of(t[k], bytes[k]);
+        st.add(range_of(t[k], bytes[k]));
     }
     for (int i = 0; i < st.n; ++i)
         for (int j = i + 1; j < st.n; ++j)
@@ -568,6 +630,7 @@ forge_status forge_adamw(const void *G, int32_t gd, void *W, void *m, void *v, f
     forge_status s;
     bool empty = false;
     if ((s = check_dtype_moment(md)) != FORGE_OK) return s;
+    if (md == FORGE_MOMENT_FP8) return FORGE_ERR_INVALID_DTYPE;
     if ((s = check_dtype_grad(gd)) != FORGE_OK) return s;
     if ((s = check_shape(0, d_in, d_out, empty)) != FORGE_OK) return s;
     if (empty) return FORGE_OK;
@@ -600,6 +663,7 @@ forge_status forge_linear_step_unfused(const void *X, const void *dY, void *W, v
     forge_status s;
     bool empty = false;
     if ((s = check_dtype_moment(md)) != FORGE_OK) return s;
+    if (md == FORGE_MOMENT_FP8) return FORGE_ERR_INVALID_DTYPE;
     if ((s = check_dtype_grad(gd)) != FORGE_OK) return s;
     if ((s = check_shape(T, d_in, d_out, empty)) != FORGE_OK) return s;
     if (empty) return FORGE_OK;

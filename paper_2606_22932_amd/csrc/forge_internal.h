@@ -31,7 +31,9 @@ struct Args {
     void *m, *v;           // moments, storage per moment dtype
     float *ms, *vs;        // int8 block scales: [ceil(d_out/256), d_in], or [d_out, ceil(d_in/64)]
     void *G;               // materialised gradient (two-kernel path only)
+    float *wr;             // fp8 weights: amax ring of W [AMAX_SLOTS]
     int T, d_in, d_out;
+    int slot;              // fp8 tensors: step % AMAX_SLOTS
     int tiles_p, tiles_q;  // tile grid (along d_out, along d_in)
     int group_p;           // raster group height in tiles (L2 reuse of operand slabs)
     Hyper h;
@@ -68,8 +70,11 @@ struct DxArgs {
 };
 
 // Moment storage: fp32, bf16, int8 with one scale per 256 rows of a column (sqrt(v)
-// stored), int8 with one scale per 64 consecutive elements of a row (v stored).
-enum MomentKind { MK_F32 = 0, MK_BF16 = 1, MK_I8 = 2, MK_I8R64 = 3 };
+// stored), int8 with one scale per 64 consecutive elements of a row (v stored), fp8 E4M3
+// with one delayed scale per tensor (m and sqrt(v) stored).
+enum MomentKind { MK_F32 = 0, MK_BF16 = 1, MK_I8 = 2, MK_I8R64 = 3, MK_FP8 = 4 };
+// fp8 tensors keep a ring of AMAX_SLOTS amax values; step t writes slot t % 4.
+constexpr int AMAX_SLOTS = 4;
 constexpr int I8_ROW_BLOCK = 64;
 // Tile epilogues of the fused kernel: the update rules (each a per-element function of G,
 // W and the rule's state), and the store-G control.
@@ -77,7 +82,8 @@ enum EpiKind {
     EPI_ADAMW = 0, EPI_STORE_BF16 = 1, EPI_STORE_F32 = 2,
     EPI_SGD = 3, EPI_SGDM = 4, EPI_ADAGRAD = 5, EPI_RMSPROP = 6, EPI_LION = 7,
     EPI_NADAM = 8, EPI_RADAM = 9, EPI_ADAMAX = 10, EPI_MUON = 11,
-    EPI_COUNT = 12
+    EPI_ADAMW_WFP8 = 12,   // AdamW with W stored as fp8 E4M3 (per-tensor delayed scale)
+    EPI_COUNT = 13
 };
 
 struct TileShape { int rows, cols, tokens; };
@@ -92,6 +98,8 @@ hipError_t launch_fused_group(const Args *a, int n, int moment_kind, hipStream_t
 // The fused step with update rule `epi` (any EpiKind but the store-G ones) on fp32 or bf16
 // state: n matrices (1 <= n <= MAX_GROUP, none empty) in one launch.
 hipError_t launch_fused_rule(const Args *a, int n, int epi, int moment_kind, hipStream_t stream);
+// AdamW with fp8 weights (and bf16 or fp8 moments): n matrices in one launch.
+hipError_t launch_fused_wfp8(const Args *a, int n, int moment_kind, hipStream_t stream);
 hipError_t launch_wgrad(const Args &a, int grad_f32, hipStream_t stream);
 hipError_t launch_adamw(const Args &a, int moment_kind, int grad_f32, hipStream_t stream);
 // dX = sum of dY_s W_s over n segments (0 <= n <= MAX_GROUP, none with d_out == 0; n == 0

@@ -687,9 +687,211 @@ struct EpiI8Row {
     }
 };
 
-// The epilogue of (moment kind, rule): the row-block int8 layout has its own (AdamW only).
+// fp8 tensors: OCP E4M3 codes (largest finite 448, round to nearest even; the hardware
+// conversion gives NaN past 464, so values are clamped into range first) with one scale per
+// tensor, s = amax / 448, where amax is a previous step's max |x| over the tensor (delayed
+// scaling; a scale of 1 while there is no history).  Each tensor has a ring of four amax
+// slots: step t decodes with the scale of slot (t-2)%4 (the one its stored codes were written
+// with), encodes with slot (t-1)%4, max-reduces its own new values into slot t%4 and clears
+// slot (t+1)%4 for the next step, so that no slot is read while another workgroup writes it.
+struct Fp8 {
+    static __device__ __forceinline__ float scale_of(float amax) { return amax > 0.0f ? amax / 448.0f : 1.0f; }
+    static __device__ __forceinline__ float clamp(float x) { return fminf(fmaxf(x, -448.0f), 448.0f); }
+    // value of byte e of 8 packed codes
+    static __device__ __forceinline__ float decode(const u32x2_t &c, int e)
+    {
+        const int w = (int)c[e >> 2];
+        switch (e & 3) {
+        case 0: return __builtin_amdgcn_cvt_f32_fp8(w, 0);
+        case 1: return __builtin_amdgcn_cvt_f32_fp8(w, 1);
+        case 2: return __builtin_amdgcn_cvt_f32_fp8(w, 2);
+        default: return __builtin_amdgcn_cvt_f32_fp8(w, 3);
+        }
+    }
+    // 8 values (already scaled) -> 8 codes
+    static __device__ __forceinline__ u32x2_t encode8(const float (&x)[8])
+    {
+        u32x2_t c;
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            const int lo = __builtin_amdgcn_cvt_pk_fp8_f32(clamp(x[4 * k]), clamp(x[4 * k + 1]), 0, false);
+            c[k] = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(clamp(x[4 * k + 2]), clamp(x[4 * k + 3]), lo, true);
+        }
+        return c;
+    }
+    // Record a wave's amax into the slot (one atomic per wave, skipped when the slot already
+    // holds at least as much; amax >= 0, so its bit pattern orders like the value).
+    static __device__ __forceinline__ void record(float *ring, int slot, float amax, int lane)
+    {
+#pragma unroll
+        for (int d = 32; d > 0; d >>= 1) amax = fmaxf(amax, __shfl_xor(amax, d));
+        if (lane == 0) {
+            unsigned *p = reinterpret_cast<unsigned *>(ring + slot);
+            const unsigned bits = __float_as_uint(amax);
+            if (bits > __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) atomicMax(p, bits);
+        }
+    }
+};
+
+// AdamW with fp8 weights (WF8) and / or fp8 moments (MF8; m and sqrt(v) stored, the sqrt(v)
+// codes at least the smallest positive code when v' > 0); the other tensors bf16.  The
+// update reads the decoded state and runs in fp32 as everywhere else.
+template <int BP, int BQ, bool WF8, bool MF8>
+struct EpiQ {
+    using M = EpiMap<BP, BQ>;
+    static constexpr int N16W = WF8 ? 1 : M::NPASS, N8W = WF8 ? M::NPASS : 1;
+    static constexpr int N16M = MF8 ? 1 : M::NPASS, N8M = MF8 ? M::NPASS : 1;
+    u32x4_t pw16[N16W], pm16[N16M], pv16[N16M];
+    u32x2_t pw8[N8W], pm8[N8M], pv8[N8M];
+    bool first_tile = false;       // the matrix's first tile clears the next step's slots
+
+    template <int I>
+    __device__ __forceinline__ void prefetch_pass(const Args &a, int p0, int q0, int s)
+    {
+        const int rs = s / M::LPR, q = q0 + (s % M::LPR) * 8;
+        const int p = p0 + I * M::RPP + rs;
+        const u32x4_t z4 = {0u, 0u, 0u, 0u};
+        const u32x2_t z2 = {0u, 0u};
+        if constexpr (WF8) pw8[I] = z2; else pw16[I] = z4;
+        if constexpr (MF8) { pm8[I] = z2; pv8[I] = z2; } else { pm16[I] = z4; pv16[I] = z4; }
+        if (q < a.d_in && p < a.d_out) {
+            const size_t off = (size_t)p * a.d_in + q;
+            if constexpr (WF8) pw8[I] = ld_nt<u32x2_t>(reinterpret_cast<const uint8_t *>(a.W) + off);
+            else pw16[I] = ld_nt<u32x4_t>(a.W + off);
+            if constexpr (MF8) {
+                pm8[I] = ld_nt<u32x2_t>(static_cast<const uint8_t *>(a.m) + off);
+                pv8[I] = ld_nt<u32x2_t>(static_cast<const uint8_t *>(a.v) + off);
+            } else {
+                pm16[I] = ld_nt<u32x4_t>(static_cast<const uint16_t *>(a.m) + off);
+                pv16[I] = ld_nt<u32x4_t>(static_cast<const uint16_t *>(a.v) + off);
+            }
+        }
+    }
+
+    template <int I = 0>
+    __device__ __forceinline__ void prefetch(const Args &a, int p0, int q0, int s)
+    {
+        prefetch_pass<I>(a, p0, q0, s);
+        if constexpr (I + 1 < M::NPASS) prefetch<I + 1>(a, p0, q0, s);
+    }
+
+    static __device__ __forceinline__ float bf(const u32x4_t &u, int e)
+    {
+        return (e & 1) ? bf_hi(u[e >> 1]) : bf_lo(u[e >> 1]);
+    }
+
+    __device__ __forceinline__ void run(const Args &a, int p0, int q0, int s, const float *Gs)
+    {
+        const int rs = s / M::LPR, qo = (s % M::LPR) * 8, q = q0 + qo;
+        const Hyper h = a.h;
+        const int wslot = a.slot, enc = (a.slot + 3) % AMAX_SLOTS, dec = (a.slot + 2) % AMAX_SLOTS;
+        float w_dec = 1.0f, w_inv = 1.0f, m_dec = 1.0f, m_inv = 1.0f, v_dec = 1.0f, v_inv = 1.0f;
+        if constexpr (WF8) {
+            w_dec = Fp8::scale_of(a.wr[dec]);
+            w_inv = 1.0f / Fp8::scale_of(a.wr[enc]);
+        }
+        if constexpr (MF8) {
+            m_dec = Fp8::scale_of(a.ms[dec]);
+            m_inv = 1.0f / Fp8::scale_of(a.ms[enc]);
+            v_dec = Fp8::scale_of(a.vs[dec]);
+            v_inv = 1.0f / Fp8::scale_of(a.vs[enc]);
+        }
+        float aw = 0.0f, am = 0.0f, av = 0.0f;
+#pragma unroll
+        for (int i = 0; i < M::NPASS; ++i) {
+            const int p = p0 + i * M::RPP + rs;
+            const bool ok = q < a.d_in && p < a.d_out;
+            const float *gr = Gs + (i * M::RPP + rs) * M::GP + qo;
+            const f32x4_t g0 = *reinterpret_cast<const f32x4_t *>(gr);
+            const f32x4_t g1 = *reinterpret_cast<const f32x4_t *>(gr + 4);
+            float wo[8], mo[8], vo[8], ro[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const float g = e < 4 ? g0[e] : g1[e - 4];
+                const float w = WF8 ? w_dec * Fp8::decode(pw8[i], e) : bf(pw16[i], e);
+                float m0, v0;
+                if constexpr (MF8) {
+                    m0 = m_dec * Fp8::decode(pm8[i], e);
+                    const float r0 = v_dec * Fp8::decode(pv8[i], e);
+                    v0 = r0 * r0;
+                } else {
+                    m0 = bf(pm16[i], e);
+                    v0 = bf(pv16[i], e);
+                }
+                adamw_elem(g, w, m0, v0, h, wo[e], mo[e], vo[e], ro[e]);
+            }
+            if (ok) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    aw = fmaxf(aw, fabsf(wo[e]));
+                    am = fmaxf(am, fabsf(mo[e]));
+                    av = fmaxf(av, ro[e]);
+                }
+                const size_t off = (size_t)p * a.d_in + q;
+                if constexpr (WF8) {
+                    float x[8];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) x[e] = wo[e] * w_inv;
+                    st_nt<u32x2_t>(reinterpret_cast<uint8_t *>(a.W) + off, Fp8::encode8(x));
+                } else {
+                    u32x4_t wn;
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) wn[k] = pack_bf16(wo[2 * k], wo[2 * k + 1]);
+                    st_nt<u32x4_t>(a.W + off, wn);
+                }
+                if constexpr (MF8) {
+                    float xm[8], xv[8];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        xm[e] = mo[e] * m_inv;
+                        xv[e] = ro[e] * v_inv;
+                    }
+                    u32x2_t cv = Fp8::encode8(xv);
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)      // sqrt(v') > 0 never stores as zero
+                        if (ro[e] > 0.0f && ((cv[e >> 2] >> (8 * (e & 3))) & 0x7Fu) == 0u)
+                            cv[e >> 2] |= 1u << (8 * (e & 3));
+                    st_nt<u32x2_t>(static_cast<uint8_t *>(a.m) + off, Fp8::encode8(xm));
+                    st_nt<u32x2_t>(static_cast<uint8_t *>(a.v) + off, cv);
+                } else {
+                    u32x4_t mn, vn;
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        mn[k] = pack_bf16(mo[2 * k], mo[2 * k + 1]);
+                        vn[k] = pack_bf16(vo[2 * k], vo[2 * k + 1]);
+                    }
+                    st_nt<u32x4_t>(static_cast<uint16_t *>(a.m) + off, mn);
+                    st_nt<u32x4_t>(static_cast<uint16_t *>(a.v) + off, vn);
+                }
+            }
+        }
+        const int lane = s & 63;
+        if constexpr (WF8) Fp8::record(a.wr, wslot, aw, lane);
+        if constexpr (MF8) {
+            Fp8::record(a.ms, wslot, am, lane);
+            Fp8::record(a.vs, wslot, av, lane);
+        }
+        if (first_tile && s == 0) {
+            const int clr = (a.slot + 1) % AMAX_SLOTS;
+            if constexpr (WF8) a.wr[clr] = 0.0f;
+            if constexpr (MF8) {
+                a.ms[clr] = 0.0f;
+                a.vs[clr] = 0.0f;
+            }
+        }
+    }
+};
+
+template <class T> struct IsEpiQ { static constexpr bool value = false; };
+template <int BP, int BQ, bool W, bool M> struct IsEpiQ<EpiQ<BP, BQ, W, M>> { static constexpr bool value = true; };
+
+// The epilogue of (moment kind, rule): the row-block int8 layout and the fp8 encodings have
+// their own (AdamW only).
 template <int BP, int BQ, int MK, int E> struct EpiSel { using T = EpiRule<BP, BQ, MK, E>; };
 template <int BP, int BQ> struct EpiSel<BP, BQ, MK_I8R64, EPI_ADAMW> { using T = EpiI8Row<BP, BQ>; };
+template <int BP, int BQ> struct EpiSel<BP, BQ, MK_FP8, EPI_ADAMW> { using T = EpiQ<BP, BQ, false, true>; };
+template <int BP, int BQ> struct EpiSel<BP, BQ, MK_BF16, EPI_ADAMW_WFP8> { using T = EpiQ<BP, BQ, true, false>; };
+template <int BP, int BQ> struct EpiSel<BP, BQ, MK_FP8, EPI_ADAMW_WFP8> { using T = EpiQ<BP, BQ, true, true>; };
 
 // AdamW on int8 block-absmax moments (App. B scheme; blocks of 256 rows along d_out,
 // second moment stored through its square root, codes of v floored at 1).  The tile is
@@ -905,6 +1107,8 @@ __global__ void __launch_bounds__(NT, 4) fused_kernel(GroupArgs g)
     static_assert(MK != MK_I8, "int8 moments run in pipelined_i8_kernel");
     static_assert(MK != MK_I8R64 || EPI == EPI_ADAMW || EPI == EPI_STORE_BF16 || EPI == EPI_STORE_F32,
                   "row-block int8 moments: AdamW only");
+    static_assert(MK != MK_FP8 || EPI == EPI_ADAMW || EPI == EPI_ADAMW_WFP8, "fp8 moments: AdamW only");
+    static_assert(EPI != EPI_ADAMW_WFP8 || MK == MK_BF16 || MK == MK_FP8, "fp8 weights: bf16 or fp8 moments");
     using ML = Mainloop<BP, BQ, NSTAGE, TK128>;
     using EM = EpiMap<BP, BQ>;
     constexpr int MAIN = ML::LDS_BYTES > EM::GS_BYTES ? ML::LDS_BYTES : EM::GS_BYTES;
@@ -932,6 +1136,7 @@ __global__ void __launch_bounds__(NT, 4) fused_kernel(GroupArgs g)
         lds_barrier();
     } else if constexpr (EPI != EPI_STORE_BF16 && EPI != EPI_STORE_F32) {
         typename EpiSel<BP, BQ, MK, EPI>::T ep;
+        if constexpr (IsEpiQ<decltype(ep)>::value) ep.first_tile = (t == g.start[mi]);
         ep.prefetch(a, p0, q0, s);
         for (int i = 0; i < nbar; ++i) lds_barrier();
         lds_barrier();
@@ -985,6 +1190,7 @@ __global__ void __launch_bounds__(NROLE, 2) adamw_kernel(Args a)
         lds_barrier();
         ep.run(a, p0, q0, s, Gs, red);
     } else {
+        static_assert(MK != MK_FP8, "fp8 moments are stepped by the fused kernel only");
         typename EpiSel<BP, BQ, MK, EPI_ADAMW>::T ep;
         ep.prefetch(a, p0, q0, s);
         stage();
@@ -1442,6 +1648,7 @@ hipError_t launch_fused_group(const Args *a, int n, int mk, hipStream_t st)
 {
     if (mk == MK_I8) return launch_i8_pipelined(a, n, st);
     if (mk == MK_I8R64) return launch_group<BP_F, BQ_F, MK_I8R64, EPI_ADAMW>(a, n, st);
+    if (mk == MK_FP8) return launch_group<BP_F, BQ_F, MK_FP8, EPI_ADAMW>(a, n, st);
     if (mk == MK_BF16) return launch_group<BP_F, BQ_F, MK_BF16, EPI_ADAMW>(a, n, st);
     return launch_group<BP_F, BQ_F, MK_F32, EPI_ADAMW>(a, n, st);
 }
@@ -1468,6 +1675,13 @@ hipError_t launch_fused_rule(const Args *a, int n, int epi, int mk, hipStream_t 
     case EPI_MUON: return launch_rule<EPI_MUON>(a, n, mk, st);
     default: return hipErrorInvalidValue;
     }
+}
+
+hipError_t launch_fused_wfp8(const Args *a, int n, int mk, hipStream_t st)
+{
+    if (mk == MK_FP8) return launch_group<BP_F, BQ_F, MK_FP8, EPI_ADAMW_WFP8>(a, n, st);
+    if (mk == MK_BF16) return launch_group<BP_F, BQ_F, MK_BF16, EPI_ADAMW_WFP8>(a, n, st);
+    return hipErrorInvalidValue;
 }
 
 hipError_t launch_fused(const Args &a, int mk, hipStream_t st)

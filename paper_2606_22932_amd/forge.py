@@ -14,7 +14,8 @@ import threading
 
 from . import build as _build
 
-FORGE_MOMENT_F32, FORGE_MOMENT_BF16, FORGE_MOMENT_I8, FORGE_MOMENT_I8_ROW64 = 0, 1, 2, 3
+FORGE_MOMENT_F32, FORGE_MOMENT_BF16, FORGE_MOMENT_I8, FORGE_MOMENT_I8_ROW64, FORGE_MOMENT_FP8 = 0, 1, 2, 3, 4
+AMAX_SLOTS = 4
 FORGE_GRAD_BF16, FORGE_GRAD_F32 = 0, 1
 
 STATUS = {
@@ -64,6 +65,8 @@ _SIGS = {
                                   _I64, _P],
     "forge_linear_step_opt": [_P, _P, _P, _P, _P, _I64, _I64, _I64, _I32, _I32, ctypes.POINTER(forge_hparams),
                               _I64, _P],
+    "forge_linear_step_wfp8": [_P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I32, _F, _F, _F, _F, _F, _I64,
+                               _P],
     "forge_input_grad": [_P, _P, _P, _I64, _I64, _I64, _P],
     "forge_linear_backward": [_P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I32, _F, _F, _F, _F, _F,
                               _I64, _P],
@@ -137,8 +140,11 @@ def _moment_code(m, m_scale=None):
     [ceil(d_out/256), d_in] (256-row column blocks) or [d_out, ceil(d_in/64)] (64-wide row
     blocks)."""
     import torch
-    codes = {torch.float32: FORGE_MOMENT_F32, torch.bfloat16: FORGE_MOMENT_BF16}
+    codes = {torch.float32: FORGE_MOMENT_F32, torch.bfloat16: FORGE_MOMENT_BF16,
+             torch.float8_e4m3fn: FORGE_MOMENT_FP8}
     if m.dtype in codes:
+        if m.dtype == torch.float8_e4m3fn and (m_scale is None or m_scale.numel() != AMAX_SLOTS):
+            raise ValueError(f"fp8 moments need amax rings of {AMAX_SLOTS} float32 (m_scale, v_scale)")
         return codes[m.dtype]
     if m.dtype != torch.int8:
         raise TypeError(f"moments must be float32, bfloat16 or int8, got {m.dtype}")
@@ -226,6 +232,29 @@ def forge_linear_step_opt(X, dY, W, s1=None, s2=None, *, optimizer, lr, beta1=0.
                                      _ptr(s2 if ns >= 2 else None), T, d_in, d_out, OPTIMIZERS[optimizer], code,
                                      ctypes.byref(hp), int(step), _stream(stream, ref))
     _check(st, "forge_linear_step_opt")
+
+
+def forge_linear_step_wfp8(X, dY, W, w_amax, m, v, m_amax=None, v_amax=None, *, lr, beta1, beta2, eps,
+                           weight_decay, step, stream=None):
+    """The fused step with W in fp8 (float8_e4m3fn codes, amax ring ``w_amax`` of 4 float32)
+    and bf16 moments, or fp8 moments (float8_e4m3fn codes of m and sqrt(v) with their rings)."""
+    import torch
+    _dev(X, dY, W, w_amax, m, v, m_amax, v_amax)
+    if X.dtype != torch.bfloat16 or dY.dtype != torch.bfloat16 or W.dtype != torch.float8_e4m3fn:
+        raise TypeError("X, dY must be bfloat16 and W float8_e4m3fn")
+    T, d_in = X.shape
+    T2, d_out = dY.shape
+    if T2 != T or tuple(W.shape) != (d_out, d_in):
+        raise ValueError(f"shape mismatch: X {tuple(X.shape)}, dY {tuple(dY.shape)}, W {tuple(W.shape)}")
+    if w_amax.dtype != torch.float32 or w_amax.numel() != AMAX_SLOTS:
+        raise ValueError(f"w_amax must be {AMAX_SLOTS} float32")
+    code = _moment_code(m, m_amax)
+    if code not in (FORGE_MOMENT_BF16, FORGE_MOMENT_FP8):
+        raise TypeError("moments must be bfloat16 or float8_e4m3fn")
+    st = lib().forge_linear_step_wfp8(_ptr(X), _ptr(dY), _ptr(W), _ptr(w_amax), _ptr(m), _ptr(v), _ptr(m_amax),
+                                      _ptr(v_amax), T, d_in, d_out, code, lr, beta1, beta2, eps, weight_decay,
+                                      int(step), _stream(stream, W))
+    _check(st, "forge_linear_step_wfp8")
 
 
 def _group(mats):

@@ -12,7 +12,8 @@ activations and gradients):
 * ``o_proj``     T=512, 4096x4096, X std 1, dY std 1e-3, W std 0.02, bf16 moments from a
                  warm state m~N(0,1e-4), v=|N(0,1e-6)|, step 100.
 * ``mlp``        T=512, gate/up [14336x4096], down [4096x14336], as ``o_proj``.
-* ``mlp_i8``     ``mlp`` with int8 block-absmax moments.
+* ``mlp_i8``     ``mlp`` with int8 block-absmax moments (256-row column blocks, sqrt(v)).
+* ``mlp_i8r64``  ``mlp`` with int8 moments in 64-wide row blocks (v stored).
 * ``sweep``      32 decoder layers x {q,k,v,o,gate,up,down} + lm_head [128256x4096], bf16 moments.
 
 "N(0, s)" means standard deviation s.  Per-tensor seeds are ``1000*base + id`` with ids
@@ -56,7 +57,7 @@ class Workload:
     name: str
     T: int
     matrices: tuple
-    moment: str                  # "f32" | "bf16" | "i8"
+    moment: str                  # "f32" | "bf16" | "i8" | "i8r64"
     x_std: float = 1.0
     dy_std: float = 1e-3
     w_std: float = 0.02
@@ -110,6 +111,8 @@ WORKLOADS = {
                                  Matrix("down", 4096, 14336, 5)), "bf16"),
     "mlp_i8": Workload("mlp_i8", 512, (Matrix("gate", 14336, 4096, 6), Matrix("up", 14336, 4096, 7),
                                        Matrix("down", 4096, 14336, 8)), "i8"),
+    "mlp_i8r64": Workload("mlp_i8r64", 512, (Matrix("gate", 14336, 4096, 6), Matrix("up", 14336, 4096, 7),
+                                             Matrix("down", 4096, 14336, 8)), "i8r64"),
     "sweep": Workload("sweep", 512, _sweep_matrices(), "bf16"),
 }
 

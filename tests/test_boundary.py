@@ -70,7 +70,7 @@ def test_query_tile():
 
 
 def test_dtype_errors():
-    assert call_step(md=4) == DTYPE
+    assert call_step(md=5) == DTYPE
     assert call_step(md=-1) == DTYPE
     assert call_unfused(gd=2) == DTYPE
     assert lib().forge_wgrad(BASE["X"], BASE["dY"], BASE["G"], 8, 8, 8, 5, None) == DTYPE
@@ -385,7 +385,7 @@ I8R64 = 3
 def test_i8_row64_dtype_and_scale_pointers():
     assert call_step(md=I8R64, ms=0) == NULLP
     assert call_step(md=I8R64, vs=BASE["vs"] + 4) == MISAL
-    assert call_step(md=4) == DTYPE
+    assert call_step(md=5) == DTYPE
     # the rule API takes fp32 / bf16 state only
     assert call_opt("adamw", md=I8R64) == DTYPE
 
@@ -399,3 +399,52 @@ def test_i8_row64_scale_extent_is_the_row_layout():
     assert call_step(md=I8, vs=vs) == NODEV
     assert call_step(md=I8R64) == NODEV
     assert call_unfused(md=I8R64) == NODEV
+
+
+# ----------------------------------------------------------------------------- fp8 encodings
+
+FP8 = 4
+
+
+def call_wfp8(T=64, d_in=128, d_out=256, md=BF16, w_amax=60 * GiB + 1024, **over):
+    a = dict(BASE)
+    a.update({k: v for k, v in over.items() if k in a})
+    hp = dict(HP)
+    hp.update({k: v for k, v in over.items() if k in hp})
+    return lib().forge_linear_step_wfp8(a["X"], a["dY"], a["W"], w_amax, a["m"], a["v"], a["ms"], a["vs"], T, d_in,
+                                        d_out, md, hp["lr"], hp["beta1"], hp["beta2"], hp["eps"], hp["wd"],
+                                        hp["step"], None)
+
+
+def test_fp8_moment_rings_are_checked():
+    assert call_step(md=FP8, ms=0) == NULLP
+    assert call_step(md=FP8, vs=BASE["vs"] + 8) == MISAL
+    assert call_step(md=FP8, vs=BASE["ms"]) == ALIAS               # the two 16-byte rings overlap
+    assert call_adamw_dtype(FP8) == DTYPE
+    assert call_unfused(md=FP8) == DTYPE
+
+
+def call_adamw_dtype(md):
+    a = BASE
+    return lib().forge_adamw(a["G"], 0, a["W"], a["m"], a["v"], a["ms"], a["vs"], 128, 256, md, 1e-3, 0.9, 0.999,
+                             1e-8, 0.1, 1, None)
+
+
+def test_fp8_weight_entry_point_errors():
+    assert call_wfp8(md=0) == DTYPE
+    assert call_wfp8(md=I8) == DTYPE
+    assert call_wfp8(w_amax=0) == NULLP
+    assert call_wfp8(w_amax=60 * GiB + 4) == MISAL
+    assert call_wfp8(md=FP8, ms=0) == NULLP
+    assert call_wfp8(w_amax=BASE["W"] + 64) == ALIAS
+    assert call_wfp8(m=BASE["W"] + 128 * 256 - 16) == ALIAS       # fp8 W is 1 byte per element
+    assert call_wfp8(step=0) == HYPER
+    assert call_wfp8(d_in=0) == OK
+
+
+@pytest.mark.skipif(_gpu_visible(), reason="on a GPU machine a valid call would launch on fake pointers")
+def test_fp8_valid_arguments_reach_the_device_check():
+    assert call_step(md=FP8) == NODEV
+    assert call_wfp8() == NODEV
+    assert call_wfp8(md=FP8) == NODEV
+    assert call_wfp8(m=BASE["W"] + 128 * 256) == NODEV           # right after a 1-byte-per-element W

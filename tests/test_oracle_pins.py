@@ -724,3 +724,93 @@ def test_i8_row64_step_reads_unquantized_state_for_the_weight():
     # and the stored state is that unquantised state, re-quantised
     qm, sm = oracle.quantize_i8_row64(m1, second_moment=False)
     assert np.array_equal(qm, out["m"]) and np.array_equal(sm, out["m_scale"])
+
+
+# ------------------------------------------------------------------------- fp8 (E4M3) encodings
+
+def test_e4m3_code_table_facts():
+    """OCP E4M3: codes 0..126 are the finite non-negative values in increasing order, from 0
+    through the smallest subnormal 2^-9 and the smallest normal 2^-6 (code 8) to 448 (code
+    126); 127 is NaN; the sign bit mirrors them; every finite code round-trips."""
+    vals = oracle.e4m3_decode(np.arange(256, dtype=np.uint8))
+    pos = vals[:127]
+    assert pos[0] == 0.0 and pos[1] == 2.0 ** -9 and pos[8] == 2.0 ** -6 and pos[126] == 448.0
+    assert np.all(np.diff(pos) > 0)
+    assert np.isnan(vals[127]) and np.isnan(vals[255])
+    np.testing.assert_array_equal(vals[128:255], -pos)
+    codes = np.concatenate([np.arange(127), np.arange(128, 255)]).astype(np.uint8)
+    assert np.array_equal(oracle.e4m3_encode(vals[codes].astype(np.float32)), codes)
+
+
+def test_e4m3_encode_is_nearest_even_by_brute_force():
+    rng = np.random.default_rng(15)
+    pos = oracle.e4m3_decode(np.arange(127, dtype=np.uint8))
+    mids = (0.5 * (pos[1:] + pos[:-1])).astype(np.float32)           # exact ties (representable in fp32)
+    x = np.concatenate([mids, -mids, (rng.random(4000) * 448).astype(np.float32),
+                        (2.0 ** rng.uniform(-14, 8.8, 4000)).astype(np.float32)])
+    got = oracle.e4m3_encode(x)
+    for xi, c in zip(x, got):
+        a = abs(float(xi))
+        d = np.abs(pos - a)
+        best = np.flatnonzero(d == d.min())
+        want = best[0] if len(best) == 1 else best[best % 2 == 0][0]   # tie: even code
+        assert (c & 0x7F) == want and (c >> 7) == (1 if np.signbit(xi) else 0), (xi, c, want)
+
+
+def _fp8_state(d_out, d_in, seed):
+    rng = np.random.default_rng(seed)
+    G = rng.standard_normal((d_out, d_in)) * 0.02
+    W = bf16_rand((d_out, d_in), 0.02, seed)
+    z = np.zeros((d_out, d_in), np.uint8)
+    return G, W, z, z.copy(), np.zeros(4, np.float32), np.zeros(4, np.float32)
+
+
+def test_fp8_cold_start_and_ring_slots():
+    """Step 1 from a zero ring encodes with scale 1, records max|m'| and max sqrt(v') into
+    slot 1 and clears slot 2; step 2 encodes with slot 1's scale, so the tensor's largest
+    value lands on 448 (or saturates there)."""
+    G, W, m, v, mr, vr = _fp8_state(6, 40, 16)
+    mr[2] = vr[2] = 123.0                      # stale content the step must clear
+    o1 = oracle.adamw_fp8(G, W, m, v, w_fp8=False, m_fp8=True, m_ring=mr, v_ring=vr, step=1, **HP)
+    m1 = o1["m64"].astype(np.float32)
+    assert o1["m_ring"][1] == np.abs(m1).max() and o1["v_ring"][1] == np.sqrt(o1["v64"]).astype(np.float32).max()
+    assert o1["m_ring"][2] == 0.0 and o1["v_ring"][2] == 0.0
+    np.testing.assert_array_equal(o1["m"], oracle.e4m3_encode(np.clip(m1, -448, 448)))   # scale 1
+    o2 = oracle.adamw_fp8(G, o1["W"], o1["m"], o1["v"], w_fp8=False, m_fp8=True, m_ring=o1["m_ring"],
+                          v_ring=o1["v_ring"], step=2, **HP)
+    s = np.float32(o1["m_ring"][1] / np.float32(448.0))
+    np.testing.assert_array_equal(o2["qm"], (o2["m64"].astype(np.float32) / s).astype(np.float64))
+    big = np.abs(o2["qm"]) >= 448.0
+    assert np.all((o2["m"][big] & 0x7F) == 126)          # at or beyond last step's amax: the top code
+    # step 2 decoded step 1's codes with scale 1 (slot 0 empty)
+    dec = oracle.e4m3_decode(o1["m"])
+    np.testing.assert_allclose(o2["m64"], f32(0.9) * dec + (1 - f32(0.9)) * G, rtol=1e-15)
+
+
+def test_fp8_second_moment_floor_and_sqrt_storage():
+    G, W, m, v, mr, vr = _fp8_state(4, 24, 17)
+    G[0, 0] = 1e-12                            # sqrt(v') ~ 3e-14: far below the smallest code
+    o = oracle.adamw_fp8(G, W, m, v, w_fp8=False, m_fp8=True, m_ring=mr, v_ring=vr, step=1, **HP)
+    assert o["v"][0, 0] == 1
+    ok = o["v"] != 1
+    np.testing.assert_array_equal(o["v"][ok], oracle.e4m3_encode(np.sqrt(o["v64"]).astype(np.float32))[ok])
+
+
+def test_fp8_weight_update_reads_decoded_state():
+    G, W, m, v, mr, vr = _fp8_state(5, 32, 18)
+    wr = np.zeros(4, np.float32)
+    Wc = oracle.e4m3_encode(np.clip(oracle.bf16_bits_to_f64(W).astype(np.float32) * 100, -448, 448))
+    wr[3] = np.float32(448.0 / 100 * 448) / 1.0        # slot (t-2)%4 for t = 5: scale 448/100
+    wr[0] = wr[3]
+    mc = oracle.e4m3_encode(np.full((5, 32), 0.5, np.float32))
+    vc = oracle.e4m3_encode(np.full((5, 32), 0.25, np.float32))
+    mr[3] = vr[3] = np.float32(448.0 * 1e-3)             # decode scale 1e-3
+    o = oracle.adamw_fp8(G, Wc, mc, vc, w_fp8=True, m_fp8=True, w_ring=wr, m_ring=mr, v_ring=vr, step=5, **HP)
+    sw = np.float32(wr[3] / np.float32(448.0))
+    W0 = sw * oracle.e4m3_decode(Wc)
+    m0 = np.float32(1e-3) * oracle.e4m3_decode(mc)
+    v0 = (np.float32(1e-3) * oracle.e4m3_decode(vc)) ** 2
+    W1, m1, v1 = oracle.adamw_f64(G, W0, m0, v0, step=5, **HP)
+    np.testing.assert_allclose(o["W64"], W1, rtol=1e-14)
+    np.testing.assert_allclose(o["m64"], m1, rtol=1e-14)
+    np.testing.assert_allclose(o["v64"], v1, rtol=1e-14)
