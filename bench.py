@@ -34,12 +34,12 @@ COPY_BYTES = 1 << 30           # size of the calibration copy (--copy-calibratio
 # sources whose sha256 is recorded: after any change to them the figure is reported as null.
 TRAFFIC = {
     "sweep": {
-        "source_sha256": "e8a0c54101a87726a11632ad0929ce72932d665a5f87f5818928956c11b250df",
-        "fetch_kib_per_launch": 207370.6,     # FETCH_SIZE, mean over the 129 launches of a step
-        "write_kib_per_launch": 340911.7,     # WRITE_SIZE
-        "fetch_scale": 1.99994,               # 1 GiB copy: FETCH_SIZE reads 524303 KiB
+        "source_sha256": "5508db4454139565480a5dbd7f515b9dfd66d5b13c2b3f51e93ca70a8adb008c",
+        "fetch_kib_per_launch": 208590.5,     # FETCH_SIZE, mean over the 129 launches of a step
+        "write_kib_per_launch": 340902.7,     # WRITE_SIZE
+        "fetch_scale": 1.99994,               # 1 GiB copy: FETCH_SIZE reads 524302 KiB
         "write_scale": 1.0,                   # 1 GiB copy: WRITE_SIZE reads 1048576 KiB
-        "bytes_per_launch": 773776101,        # (fetch * fetch_scale + write * write_scale) KiB
+        "bytes_per_launch": 776264893,        # (fetch * fetch_scale + write * write_scale) KiB
     },
 }
 
