@@ -1202,13 +1202,13 @@ __global__ void __launch_bounds__(NROLE, 2) adamw_kernel(Args a)
 // ------------------------------------------------ int8 moments: tiles pipelined per CU
 //
 // One workgroup per CU steps a sequence of 256x64 tiles.  Its four math waves run the
-// mainloop of tile k while its four stream waves finish tile k-1 (App. B update of W,
-// block absmax, re-quantisation of m and sqrt(v)) and load tile k's state for the next
-// period.  G reaches the stream waves through an LDS stage of its own, written by the
-// math waves between the barriers H1 and H2 that close each period and read by the
-// stream waves during the next period, before its H1.  Every workgroup barrier is
-// executed by all eight waves: a period has nb = max(nch, 2) barriers (the mainloop's
-// chunk barriers, padded), then H1 and H2.
+// mainloop of tile k while its stream waves finish tile k-1 (App. B update of W, block
+// absmax, re-quantisation of m and sqrt(v)) and load tile k's state for the next period.
+// G reaches the stream waves through an LDS stage of its own, written by the math waves
+// between the barriers H1 and H2 that close each period and read by the stream waves
+// during the next period, before its H1; pass 1 leaves m' in that stage in place of g for
+// pass 2.  Every workgroup barrier is executed by all waves: a period has nb = max(nch, 2)
+// barriers (the mainloop's chunk barriers, padded), then H1 and H2.
 
 // Byte offset of element (p, q) of a [rows, ld] tensor with `eb`-byte elements, or an
 // offset past every buffer end (reads zero) when the element lies outside the tensor.
@@ -1233,6 +1233,7 @@ struct StreamI8 {
     u32x2_t cm[NPASS], cv[NPASS];                       // m and sqrt(v) codes (8 int8 each)
     float sm[8], sv[8];                                 // the block's old scales of this lane's columns
     float am[8], av[8];                                 // absmax partials
+    float rv[NPASS][8];                                 // sqrt(v') of each pass, for pass 2
     float rcm[8], rcv[8];                               // reciprocals of the new scales
 
     // Loads of the state of tile (p0, q0) of matrix a: row I of every pass, then the scales.
@@ -1309,6 +1310,15 @@ struct StreamI8 {
         }
     }
 
+    // m' of row I of this lane back into the LDS stage, over its g.
+    template <int I>
+    static __device__ __forceinline__ void put_row(float *Gs, int s, const float x[8])
+    {
+        float *gr = Gs + (I * M::RPP + s / M::LPR) * M::GP + (s % M::LPR) * 8;
+        *reinterpret_cast<f32x4_t *>(gr) = f32x4_t{x[0], x[1], x[2], x[3]};
+        *reinterpret_cast<f32x4_t *>(gr + 4) = f32x4_t{x[4], x[5], x[6], x[7]};
+    }
+
     // The element's state before and after the step (App. B: m = s_m q_m, v = (s_v q_v)^2).
     __device__ __forceinline__ void state_at(const Hyper &h, int i, float g, int e, float &w1, float &m1,
                                              float &v1, float &rv1) const
@@ -1319,30 +1329,42 @@ struct StreamI8 {
         adamw_elem(g, w0, m0, r0 * r0, h, w1, m1, v1, rv1);
     }
 
-    // Pass 1, row I of tile (p0, q0): new W (from the unquantised fp32 state), absmax;
-    // then W's registers take row I of the next tile (pn, qn) of matrix an.
+    // Pass 1, row I of tile (p0, q0), from the unquantised fp32 state: W' is stored, m'
+    // replaces g in the LDS stage and sqrt(v') stays in registers, both waiting for the
+    // block's new scales; absmax partials.  The row's W and code registers are then free
+    // and take row I of the next tile (pn, qn) of matrix an, and after the last row the
+    // scale registers take that tile's scales.
     template <int I>
-    __device__ __forceinline__ void pass1(const Args &a, int p0, int q0, int s, const float *Gs,
+    __device__ __forceinline__ void pass1(const Args &a, int p0, int q0, int s, float *Gs,
                                           const Args &an, int pn, int qn, bool refill)
     {
         const int p = p0 + I * M::RPP + s / M::LPR, q = q0 + (s % M::LPR) * 8;
-        float g[8], wo[8];
+        float g[8], wo[8], mo[8];
         g_row<I>(Gs, s, g);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-            float m1, v1, rv1;
-            state_at(a.h, I, g[e], e, wo[e], m1, v1, rv1);
-            am[e] = fmaxf(am[e], fabsf(m1));
-            av[e] = fmaxf(av[e], rv1);
+            float v1;
+            state_at(a.h, I, g[e], e, wo[e], mo[e], v1, rv[I][e]);
+            am[e] = fmaxf(am[e], fabsf(mo[e]));
+            av[e] = fmaxf(av[e], rv[I][e]);
         }
+        put_row<I>(Gs, s, mo);
         if (p < a.d_out && q < a.d_in) {
             u32x4_t wn;
 #pragma unroll
             for (int k = 0; k < 4; ++k) wn[k] = pack_bf16(wo[2 * k], wo[2 * k + 1]);
             st_nt<u32x4_t>(a.W + (size_t)p * a.d_in + q, wn);
         }
-        asm volatile("" ::"v"(w[I]));
-        if (refill) load_w<I>(an, pn, qn, s);
+        asm volatile("" ::"v"(w[I]), "v"(cm[I]), "v"(cv[I]));
+        if (refill) {
+            load_w<I>(an, pn, qn, s);
+            load_codes<I>(an, pn, qn, s);
+            if constexpr (I + 1 == NPASS) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) asm volatile("" ::"v"(sm[e]), "v"(sv[e]));
+                load_scales(an, pn, qn, s);
+            }
+        }
     }
 
     // Block absmax of this lane's columns over its rows: within the wave, then (through
@@ -1368,50 +1390,54 @@ struct StreamI8 {
         }
     }
 
-    // After the barrier: the block's new scales s = absmax / 127 (stored), kept as reciprocals.
-    __device__ __forceinline__ void scales(const Args &a, int p0, int q0, int s, const float *red)
+    // After the barrier: the block's new scales s = absmax / 127, one per thread of the
+    // first 2*BQ (m for the first BQ columns, sqrt(v) for the next): the column's absmax
+    // over the stream waves' partials; s is stored and its reciprocal put in LDS.
+    __device__ __forceinline__ void scales(const Args &a, int p0, int q0, int s, float *red)
     {
-        const int rs = s / M::LPR, qo = (s % M::LPR) * 8, q = q0 + qo;
-        float scm[8], scv[8];
+        if (s < 2 * BQ_I8) {
+            const int kind = s / BQ_I8, c = s % BQ_I8;
+            const float *r = red + kind * NSW * BQ_I8 + c;
+            float x = r[0];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            float xm = red[qo + e], xv = red[NSW * BQ_I8 + qo + e];
-#pragma unroll
-            for (int wv = 1; wv < NSW; ++wv) {
-                xm = fmaxf(xm, red[wv * BQ_I8 + qo + e]);
-                xv = fmaxf(xv, red[NSW * BQ_I8 + wv * BQ_I8 + qo + e]);
+            for (int wv = 1; wv < NSW; ++wv) x = fmaxf(x, r[wv * BQ_I8]);
+            const float sc = x / 127.0f;
+            red[2 * NSW * BQ_I8 + s] = sc > 0.0f ? __builtin_amdgcn_rcpf(sc) : 0.0f;
+            if (q0 + c < a.d_in) {
+                float *dst = kind ? a.vs : a.ms;
+                st_nt<float>(dst + (size_t)(p0 / I8_BLOCK) * a.d_in + q0 + c, sc);
             }
-            scm[e] = xm / 127.0f;
-            scv[e] = xv / 127.0f;
-            rcm[e] = scm[e] > 0.0f ? __builtin_amdgcn_rcpf(scm[e]) : 0.0f;
-            rcv[e] = scv[e] > 0.0f ? __builtin_amdgcn_rcpf(scv[e]) : 0.0f;
-        }
-        if (rs == 0 && q < a.d_in) {
-            const size_t so = (size_t)(p0 / I8_BLOCK) * a.d_in + q;
-            st_nt<f32x4_t>(a.ms + so, f32x4_t{scm[0], scm[1], scm[2], scm[3]});
-            st_nt<f32x4_t>(a.ms + so + 4, f32x4_t{scm[4], scm[5], scm[6], scm[7]});
-            st_nt<f32x4_t>(a.vs + so, f32x4_t{scv[0], scv[1], scv[2], scv[3]});
-            st_nt<f32x4_t>(a.vs + so + 4, f32x4_t{scv[4], scv[5], scv[6], scv[7]});
         }
     }
 
-    // Pass 2, row I: recompute m' and sqrt(v') (the same instructions as pass 1), re-quantise
-    // them against the new scales (v codes at least 1 in a non-zero block), store the codes;
-    // then the code registers take row I of the next tile.
+    // After the next barrier: the reciprocals of this lane's eight columns.
+    __device__ __forceinline__ void recips(int s, const float *red)
+    {
+        const float *r = red + 2 * NSW * BQ_I8 + (s % M::LPR) * 8;
+        const f32x4_t m0 = *reinterpret_cast<const f32x4_t *>(r);
+        const f32x4_t m1 = *reinterpret_cast<const f32x4_t *>(r + 4);
+        const f32x4_t v0 = *reinterpret_cast<const f32x4_t *>(r + BQ_I8);
+        const f32x4_t v1 = *reinterpret_cast<const f32x4_t *>(r + BQ_I8 + 4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            rcm[e] = m0[e]; rcm[e + 4] = m1[e];
+            rcv[e] = v0[e]; rcv[e + 4] = v1[e];
+        }
+    }
+
+    // Pass 2, row I: m' (from the LDS stage) and sqrt(v') (from registers) quantised
+    // against the new scales (v codes at least 1 in a non-zero block); the codes are stored.
     template <int I>
-    __device__ __forceinline__ void pass2(const Args &a, int p0, int q0, int s, const float *Gs,
-                                          const Args &an, int pn, int qn, bool refill)
+    __device__ __forceinline__ void pass2(const Args &a, int p0, int q0, int s, const float *Gs)
     {
         const int p = p0 + I * M::RPP + s / M::LPR, q = q0 + (s % M::LPR) * 8;
         uint32_t qm2[2] = {0u, 0u}, qv2[2] = {0u, 0u};
-        float g[8];
-        g_row<I>(Gs, s, g);
+        float mo[8];
+        g_row<I>(Gs, s, mo);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-            float w1, m1, v1, rv1;
-            state_at(a.h, I, g[e], e, w1, m1, v1, rv1);
-            const float qm = fminf(fmaxf(__builtin_rintf(m1 * rcm[e]), -127.0f), 127.0f);
-            float qv = fminf(fmaxf(__builtin_rintf(rv1 * rcv[e]), 1.0f), 127.0f);
+            const float qm = fminf(fmaxf(__builtin_rintf(mo[e] * rcm[e]), -127.0f), 127.0f);
+            float qv = fminf(fmaxf(__builtin_rintf(rv[I][e] * rcv[e]), 1.0f), 127.0f);
             if (!(rcv[e] > 0.0f)) qv = 0.0f;
             qm2[e >> 2] |= ((uint32_t)(int32_t)qm & 0xFFu) << (8 * (e & 3));
             qv2[e >> 2] |= ((uint32_t)(int32_t)qv & 0xFFu) << (8 * (e & 3));
@@ -1421,15 +1447,14 @@ struct StreamI8 {
             st_nt<u32x2_t>(static_cast<int8_t *>(a.m) + off, u32x2_t{qm2[0], qm2[1]});
             st_nt<u32x2_t>(static_cast<int8_t *>(a.v) + off, u32x2_t{qv2[0], qv2[1]});
         }
-        asm volatile("" ::"v"(cm[I]), "v"(cv[I]));
-        if (refill) load_codes<I>(an, pn, qn, s);
     }
 
-    // The whole epilogue of one tile, spread over nb barriers: pass-1 rows over the first
-    // half (the last of those barriers separates the absmax partials from their reads),
-    // pass-2 rows over the second half.  Executes exactly nb barriers.
+    // The whole epilogue of one tile, spread over nb >= 2 barriers: pass-1 rows over the
+    // first half (its last barrier, A, separates the absmax partials from their reads), the
+    // scales between A and the next barrier B, pass-2 rows over the rest.  Executes exactly
+    // nb barriers.
     template <int I = 0>
-    __device__ __forceinline__ void p1_all(const Args &a, int p0, int q0, int s, const float *Gs,
+    __device__ __forceinline__ void p1_all(const Args &a, int p0, int q0, int s, float *Gs,
                                            const Args &an, int pn, int qn, bool refill, int half, int &done,
                                            float *red)
     {
@@ -1440,23 +1465,22 @@ struct StreamI8 {
         } else {
             for (; done < half - 1; ++done) lds_barrier();
             partials(s, red);
-            lds_barrier();
+            lds_barrier();                                   // A
             ++done;
         }
     }
     template <int I = 0>
-    __device__ __forceinline__ void p2_all(const Args &a, int p0, int q0, int s, const float *Gs,
-                                           const Args &an, int pn, int qn, bool refill, int half, int nb,
-                                           int &done)
+    __device__ __forceinline__ void p2_all(const Args &a, int p0, int q0, int s, const float *Gs, int half,
+                                           int nb, int &done)
     {
-        pass2<I>(a, p0, q0, s, Gs, an, pn, qn, refill);
-        const int t = half + ((I + 1) * (nb - half)) / NPASS;
+        pass2<I>(a, p0, q0, s, Gs);
+        const int t = half + 1 + ((I + 1) * (nb - half - 1)) / NPASS;
         for (; done < t; ++done) lds_barrier();
-        if constexpr (I + 1 < NPASS) p2_all<I + 1>(a, p0, q0, s, Gs, an, pn, qn, refill, half, nb, done);
+        if constexpr (I + 1 < NPASS) p2_all<I + 1>(a, p0, q0, s, Gs, half, nb, done);
     }
-    // G of the tile stays in its LDS stage until this returns (the math waves overwrite
-    // it only after the next H1).
-    __device__ __forceinline__ void tile(const Args &a, int p0, int q0, int s, const float *Gs,
+    // G of the tile stays in its LDS stage (m' after pass 1) until this returns (the math
+    // waves overwrite it only after the next H1).
+    __device__ __forceinline__ void tile(const Args &a, int p0, int q0, int s, float *Gs,
                                          const Args &an, int pn, int qn, bool refill, int nb, float *red)
     {
         const int half = nb / 2;
@@ -1464,19 +1488,10 @@ struct StreamI8 {
         reset();
         p1_all(a, p0, q0, s, Gs, an, pn, qn, refill, half, done, red);
         scales(a, p0, q0, s, red);
-        // Hide the codes and scales from common-subexpression elimination, so that pass 2
-        // recomputes m' and sqrt(v') (bit-identical: the same instructions) instead of
-        // keeping 128 dequantised values from pass 1 alive.
-#pragma unroll
-        for (int i = 0; i < NPASS; ++i) asm volatile("" : "+v"(cm[i]), "+v"(cv[i]));
-#pragma unroll
-        for (int e = 0; e < 8; ++e) asm volatile("" : "+v"(sm[e]), "+v"(sv[e]));
-        p2_all(a, p0, q0, s, Gs, an, pn, qn, refill, half, nb, done);
-        if (refill) {
-#pragma unroll
-            for (int e = 0; e < 8; ++e) asm volatile("" ::"v"(sm[e]), "v"(sv[e]));
-            load_scales(an, pn, qn, s);
-        }
+        lds_barrier();                                       // B
+        ++done;
+        recips(s, red);
+        p2_all(a, p0, q0, s, Gs, half, nb, done);
     }
 };
 
@@ -1487,7 +1502,7 @@ __global__ void __launch_bounds__(NT_I8P, NT_I8P / 256) pipelined_i8_kernel(Grou
 {
     using ML = Mainloop<BP_I8, BQ_I8, NS_I8P, 32>;
     using EM = EpiMap<BP_I8, BQ_I8, NSW_I8P * 64>;
-    constexpr int RED_BYTES = 2 * NSW_I8P * BQ_I8 * 4;
+    constexpr int RED_BYTES = (2 * NSW_I8P * BQ_I8 + 2 * BQ_I8) * 4;   // absmax partials, then reciprocals
     __shared__ __attribute__((aligned(16))) unsigned char smem[EM::GS_BYTES + ML::LDS_BYTES + RED_BYTES];
     float *Gs = reinterpret_cast<float *>(smem);
     unsigned char *ring = smem + EM::GS_BYTES;
