@@ -34,14 +34,28 @@ COPY_BYTES = 1 << 30           # size of the calibration copy (--copy-calibratio
 # sources whose sha256 is recorded: after any change to them the figure is reported as null.
 TRAFFIC = {
     "sweep": {
-        "source_sha256": "5508db4454139565480a5dbd7f515b9dfd66d5b13c2b3f51e93ca70a8adb008c",
-        "fetch_kib_per_launch": 208590.5,     # FETCH_SIZE, mean over the 129 launches of a step
-        "write_kib_per_launch": 340902.7,     # WRITE_SIZE
-        "fetch_scale": 1.99994,               # 1 GiB copy: FETCH_SIZE reads 524302 KiB
+        "source_sha256": "58dcde8e4732fd103f7ffa41d758e6d241a6dc70e98b6f910a32cc6af6f54a92",
+        "fetch_kib_per_launch": 208501.9,     # FETCH_SIZE, mean over the 129 launches of a step
+        "write_kib_per_launch": 340885.6,     # WRITE_SIZE
+        "fetch_scale": 1.99995,               # 1 GiB copy: FETCH_SIZE reads 524302 KiB
         "write_scale": 1.0,                   # 1 GiB copy: WRITE_SIZE reads 1048576 KiB
-        "bytes_per_launch": 776264893,        # (fetch * fetch_scale + write * write_scale) KiB
+        "bytes_per_launch": 776066943,        # (fetch * fetch_scale + write * write_scale) KiB
+    },
+    "mlp_i8": {
+        "source_sha256": "58dcde8e4732fd103f7ffa41d758e6d241a6dc70e98b6f910a32cc6af6f54a92",
+        "fetch_kib_per_launch": 165891.5,     # mean over the 3 launches (gate, up, down)
+        "write_kib_per_launch": 256329.4,
+        "fetch_scale": 1.99995,
+        "write_scale": 1.0,
+        "bytes_per_launch": 602217886,
     },
 }
+
+# Default (warmup, timed) steps per workload when --steps / --warmup are not given: the
+# sweep's 20 ms steps need few; the single-matrix and MLP workloads get enough steps for
+# about 0.1 s of warmup and 0.2 s of timed work, so that clocks and TLBs are warm.
+DEFAULT_STEPS = {"sweep": (3, 10), "o_proj": (2000, 4000), "mlp": (200, 400), "mlp_i8": (200, 300),
+                 "mlp_i8r64": (200, 400)}
 
 
 def log(*a):
@@ -169,8 +183,8 @@ def cpu_baseline(wl, device, budget_s=10.0):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=None, help="timed steps (default: per workload)")
+    ap.add_argument("--warmup", type=int, default=None, help="untimed warmup steps (default: per workload)")
     ap.add_argument("--workload", default="sweep", choices=["sweep", "o_proj", "mlp", "mlp_i8", "mlp_i8r64"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
@@ -189,6 +203,17 @@ def main():
     if args.gpus != 1 or world != 1:
         print("bench.py measures the fused step on one GPU only: the step has no cross-GPU "
               "work (run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    if args.micro:
+        args.warmup = 3 if args.warmup is None else args.warmup
+        args.steps = 10 if args.steps is None else args.steps
+    else:
+        w0, k0 = DEFAULT_STEPS[args.workload]
+        args.warmup = w0 if args.warmup is None else args.warmup
+        args.steps = k0 if args.steps is None else args.steps
+    if args.steps < 1 or args.warmup < 0:
+        print("--steps must be at least 1 and --warmup at least 0", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -234,8 +259,9 @@ def main():
     log(f"fused: {ms:.3f} ms/step, {value:.1f} GB/s, kernel-time {kern_gbs:.1f} GB/s, "
         f"MFMA {flops / (ms * 1e-3) / 1e12:.1f} TF/s, wall {wall:.1f} ms")
 
-    tr = measured_traffic(args.workload)
+    tr = measured_traffic(args.workload) if args.tokens is None else None   # measured at the workload's T
     traffic = None if tr is None else tr["bytes_per_launch"]
+    kernel = "pipelined_i8_kernel" if wl.moment == "i8" else "fused_kernel"
     out = {
         "metric": "fused dW+AdamW step: HBM GB/s & % roofline; ms per Llama-8B linear sweep",
         "value": round(value, 2),
@@ -267,7 +293,7 @@ def main():
             "unit": "GB/s",
             "frac": round(kern_gbs / HBM_PEAK_GBS, 4),
             "traffic": traffic,
-            "kernel": "fused_kernel (forge_linear_step_grouped)",
+            "kernel": f"{kernel} (forge_linear_step_grouped)",
             "algorithmic_bytes_per_launch": round(fused_b / len(launches)),
             "avg_launch_us": round(avg_launch_ms * 1e3, 3),
             "launches_per_step": len(launches),
