@@ -20,7 +20,9 @@ def _say(*a):
 
 
 # (T, d_in, d_out): several tiles, ragged tiles on both axes, ragged token chunks,
-# the empty token axis and the smallest legal shape.
+# the empty token axis and the smallest legal shape; long token axes, where the int8
+# column-block kernel walks its tiles in raster groups of 2 and of 1 tile rows (a group's
+# dY slabs are kept near 2 MB).
 SMALL = [
     (128, 256, 256),
     (77, 328, 200),
@@ -29,6 +31,8 @@ SMALL = [
     (0, 64, 32),
     (512, 384, 520),
     (200, 1032, 776),
+    (2048, 200, 1032),
+    (4100, 136, 776),
 ]
 
 
