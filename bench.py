@@ -332,10 +332,13 @@ def main():
         mats = launches = None
         torch.cuda.synchronize()
         torch.cuda.empty_cache()
-        log("measuring HBM ceilings (read / write / copy / in-place read-modify-write of 3 streams)")
+        log("measuring HBM ceilings (read / write / copy / in-place read-modify-write of 3 streams, "
+            "in address order and in 128x128 tiles)")
         c = hbm_ceilings()
         if c is not None:
             c["fused_over_rmw3"] = round(kern_gbs / c["rmw3"], 4)
+            if "rmw3_tile" in c:
+                c["fused_over_rmw3_tile"] = round(kern_gbs / c["rmw3_tile"], 4)
             out["hbm_ceiling"] = c
             log(f"ceilings: {c}")
 

@@ -1,13 +1,18 @@
 // hbm_ceiling -- measured HBM bandwidth of this device for the access mixes of the fused
 // step, used as context for its roofline (the published peak stays the reference):
-//   read     one stream read
-//   write    one stream written
-//   copy     one stream read, another written
-//   rmw3     three streams each read and written in place (the state traffic of a fused
-//            step: W, m and v read and written back)
-// Buffers are sized well past the memory-side cache; 16 bytes per lane, grid-stride,
-// non-temporal; each figure is the best over grids of 4-32 workgroups per CU and three
-// repetitions.  Prints one JSON object on stdout.
+//   read       one stream read
+//   write      one stream written
+//   copy       one stream read, another written
+//   rmw3       three streams each read and written in place, in address order
+//   rmw3_tile  the same three streams as bf16 [R, 4096] matrices walked in 128x128 tiles in
+//              the fused kernel's order (XCD-contiguous tile ranges, raster groups of 16
+//              tile rows): the state traffic of a fused step without its GEMM
+// Each figure is the best over a sweep of launch shapes: workgroup size, workgroups per CU
+// (down to one per two CUs), elements in flight per thread, and for the tiles how many row
+// passes a thread keeps in flight.  The sweep matters: in-place traffic runs fastest with
+// few requests in flight per CU, and a probe that only tries full occupancy understates it
+// by about 12 %.  Buffers are sized well past the memory-side cache; 16 bytes per lane,
+// non-temporal.  Prints one JSON object on stdout, with the launch shape of each best.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 #include <stdio.h>
@@ -17,37 +22,107 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 namespace {
 
+// Grid-stride kernels with U elements per thread per step, all loads before the stores.
+// The host trims n to a multiple of U * (threads in the grid).
+template <int U>
 __global__ void __launch_bounds__(256) k_read(const u32x4_t *a, size_t n, u32x4_t *sink)
 {
+    const size_t stride = (size_t)gridDim.x * blockDim.x;
     u32x4_t acc = {0u, 0u, 0u, 0u};
-    for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
-        acc ^= __builtin_nontemporal_load(a + i);
+    for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += stride * U) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) acc ^= __builtin_nontemporal_load(a + i + u * stride);
+    }
     if ((acc[0] ^ acc[1] ^ acc[2] ^ acc[3]) == 0x9e3779b9u) sink[0] = acc;   // keeps the loads
 }
 
+template <int U>
 __global__ void __launch_bounds__(256) k_write(u32x4_t *a, size_t n)
 {
+    const size_t stride = (size_t)gridDim.x * blockDim.x;
     const u32x4_t v = {1u, 2u, 3u, 4u};
-    for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
-        __builtin_nontemporal_store(v, a + i);
+    for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += stride * U) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) __builtin_nontemporal_store(v, a + i + u * stride);
+    }
 }
 
+template <int U>
 __global__ void __launch_bounds__(256) k_copy(const u32x4_t *a, u32x4_t *b, size_t n)
 {
-    for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
-        __builtin_nontemporal_store(__builtin_nontemporal_load(a + i), b + i);
+    const size_t stride = (size_t)gridDim.x * blockDim.x;
+    for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += stride * U) {
+        u32x4_t x[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) x[u] = __builtin_nontemporal_load(a + i + u * stride);
+#pragma unroll
+        for (int u = 0; u < U; ++u) __builtin_nontemporal_store(x[u], b + i + u * stride);
+    }
 }
 
+template <int U>
 __global__ void __launch_bounds__(256) k_rmw3(u32x4_t *w, u32x4_t *m, u32x4_t *v, size_t n)
 {
-    for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
-        const u32x4_t x = __builtin_nontemporal_load(w + i);
-        const u32x4_t y = __builtin_nontemporal_load(m + i);
-        const u32x4_t z = __builtin_nontemporal_load(v + i);
-        __builtin_nontemporal_store(x + 1u, w + i);
-        __builtin_nontemporal_store(y ^ x, m + i);
-        __builtin_nontemporal_store(z + y, v + i);
+    const size_t stride = (size_t)gridDim.x * blockDim.x;
+    for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += stride * U) {
+        u32x4_t x[U], y[U], z[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            x[u] = __builtin_nontemporal_load(w + i + u * stride);
+            y[u] = __builtin_nontemporal_load(m + i + u * stride);
+            z[u] = __builtin_nontemporal_load(v + i + u * stride);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            __builtin_nontemporal_store(x[u] + 1u, w + i + u * stride);
+            __builtin_nontemporal_store(y[u] ^ x[u], m + i + u * stride);
+            __builtin_nontemporal_store(z[u] + y[u], v + i + u * stride);
+        }
     }
+}
+
+constexpr int TILE_COLS16 = 4096 / 8;   // 16-byte pieces per row of a [R, 4096] bf16 matrix
+
+__device__ __forceinline__ int xcd_range(int bid, int ntiles)
+{
+    const int k = ntiles >> 3, r = ntiles & 7;
+    const int x = bid & 7, s = bid >> 3;
+    return (x < r) ? x * (k + 1) + s : r * (k + 1) + (x - r) * k + s;
+}
+
+// One 128x128 tile per workgroup of 256 threads: 16 lanes per 256-byte row segment, 16 rows
+// per pass, 8 passes; D passes of loads in flight before their stores.  Dynamic LDS
+// (unused) limits the workgroups per CU.
+template <int D>
+__global__ void __launch_bounds__(256) k_rmw3_tile(u32x4_t *w, u32x4_t *m, u32x4_t *v, int tiles_p)
+{
+    extern __shared__ unsigned char occupancy_pad[];
+    constexpr int tiles_q = TILE_COLS16 / 16, group = 16;
+    const int ntiles = tiles_p * tiles_q;
+    const int t = xcd_range((int)blockIdx.x, ntiles);
+    const int per = group * tiles_q, g = t / per, first = g * group;
+    const int gsz = min(group, tiles_p - first), within = t - g * per;
+    const int tp = first + within % gsz, tq = within / gsz;
+    const size_t r0 = (size_t)tp * 128 + threadIdx.x / 16;
+    const size_t c = (size_t)tq * 16 + threadIdx.x % 16;
+    for (int p0 = 0; p0 < 8; p0 += D) {
+        u32x4_t x[D], y[D], z[D];
+#pragma unroll
+        for (int d = 0; d < D; ++d) {
+            const size_t i = (r0 + 16 * (p0 + d)) * TILE_COLS16 + c;
+            x[d] = __builtin_nontemporal_load(w + i);
+            y[d] = __builtin_nontemporal_load(m + i);
+            z[d] = __builtin_nontemporal_load(v + i);
+        }
+#pragma unroll
+        for (int d = 0; d < D; ++d) {
+            const size_t i = (r0 + 16 * (p0 + d)) * TILE_COLS16 + c;
+            __builtin_nontemporal_store(x[d] + 1u, w + i);
+            __builtin_nontemporal_store(y[d] ^ x[d], m + i);
+            __builtin_nontemporal_store(z[d] + y[d], v + i);
+        }
+    }
+    if (threadIdx.x >= 1024) occupancy_pad[0] = 0;   // never: keeps the pad referenced
 }
 
 bool ok(hipError_t e, const char *what)
@@ -57,12 +132,89 @@ bool ok(hipError_t e, const char *what)
     return false;
 }
 
+struct Best {
+    double gbs = 0.0;
+    char shape[64] = "";
+};
+
+struct Timer {
+    hipEvent_t e0, e1;
+    bool init() { return ok(hipEventCreate(&e0), "event") && ok(hipEventCreate(&e1), "event"); }
+    // Best of `reps` runs after one warm-up run; returns ms or a negative value on error.
+    template <class F>
+    float best_ms(F &&launch, int reps)
+    {
+        float best = 1e30f;
+        for (int r = 0; r <= reps; ++r) {
+            if (!ok(hipEventRecord(e0), "record")) return -1.0f;
+            launch();
+            if (!ok(hipGetLastError(), "launch") || !ok(hipEventRecord(e1), "record") ||
+                !ok(hipEventSynchronize(e1), "sync"))
+                return -1.0f;
+            float ms = 0.0f;
+            if (!ok(hipEventElapsedTime(&ms, e0, e1), "elapsed")) return -1.0f;
+            if (r > 0 && ms < best) best = ms;
+        }
+        return best;
+    }
+};
+
+template <int U>
+bool stream_kind(int kind, u32x4_t *A, u32x4_t *B, u32x4_t *C, u32x4_t *sink, size_t n_all, int ncu,
+                 Timer &tm, Best &best)
+{
+    const int blocks[3] = {64, 128, 256};
+    const int per_cu2[5] = {1, 2, 4, 8, 32};              // workgroups per CU, times 2
+    for (int bi = 0; bi < 3; ++bi)
+        for (int gi = 0; gi < 5; ++gi) {
+            const int bs = blocks[bi], grid = ncu * per_cu2[gi] / 2;
+            const size_t chunk = (size_t)grid * bs * U;
+            const size_t n = n_all / chunk * chunk;
+            const float ms = tm.best_ms([&] {
+                if (kind == 0) k_read<U><<<grid, bs>>>(A, n, sink);
+                if (kind == 1) k_write<U><<<grid, bs>>>(A, n);
+                if (kind == 2) k_copy<U><<<grid, bs>>>(A, B, n);
+                if (kind == 3) k_rmw3<U><<<grid, bs>>>(A, B, C, n);
+            }, 2);
+            if (ms < 0.0f) return false;
+            const double streams = kind < 2 ? 1.0 : kind == 2 ? 2.0 : 6.0;
+            const double gbs = streams * (double)n * 16.0 / (ms * 1e-3) / 1e9;
+            if (gbs > best.gbs) {
+                best.gbs = gbs;
+                snprintf(best.shape, sizeof best.shape, "block %d, %.1f per CU, %d in flight", bs,
+                         per_cu2[gi] / 2.0, U);
+            }
+        }
+    return true;
+}
+
+template <int D>
+bool tile_kind(u32x4_t *A, u32x4_t *B, u32x4_t *C, int tiles_p, Timer &tm, Best &best)
+{
+    const int pads[4] = {0, 40 << 10, 80 << 10, 160 << 10};   // up to 1 workgroup per CU
+    const char *occ[4] = {"full occupancy", "4 per CU", "2 per CU", "1 per CU"};
+    const int ntiles = tiles_p * (TILE_COLS16 / 16);
+    const double bytes = 6.0 * (double)tiles_p * 128.0 * 4096.0 * 2.0;
+    for (int pi = 0; pi < 4; ++pi) {
+        const float ms = tm.best_ms([&] {
+            hipLaunchKernelGGL(k_rmw3_tile<D>, dim3(ntiles), dim3(256), pads[pi], 0, A, B, C, tiles_p);
+        }, 2);
+        if (ms < 0.0f) return false;
+        const double gbs = bytes / (ms * 1e-3) / 1e9;
+        if (gbs > best.gbs) {
+            best.gbs = gbs;
+            snprintf(best.shape, sizeof best.shape, "%s, %d passes in flight", occ[pi], D);
+        }
+    }
+    return true;
+}
+
 }  // namespace
 
 int main(int argc, char **argv)
 {
-    // bytes per stream (default 12 GiB: 36 GiB for rmw3, far past the 256 MiB MALL)
-    const size_t bytes = (argc > 1 ? strtoull(argv[1], nullptr, 10) : 12ull) << 30;
+    // bytes per stream (default 4 GiB: 12 GiB for rmw3, far past the 256 MiB MALL)
+    const size_t bytes = (argc > 1 ? strtoull(argv[1], nullptr, 10) : 4ull) << 30;
     const size_t n = bytes / 16;
     u32x4_t *A = nullptr, *B = nullptr, *C = nullptr, *sink = nullptr;
     if (!ok(hipMalloc(&A, bytes), "hipMalloc") || !ok(hipMalloc(&B, bytes), "hipMalloc") ||
@@ -73,34 +225,24 @@ int main(int argc, char **argv)
         return 1;
     int ncu = 0;
     if (!ok(hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, 0), "attribute")) return 1;
-    hipEvent_t e0, e1;
-    if (!ok(hipEventCreate(&e0), "event") || !ok(hipEventCreate(&e1), "event")) return 1;
-    const char *names[4] = {"read", "write", "copy", "rmw3"};
-    double gbs[4];
-    // the ceiling of a mix: the best of several grid sizes (workgroups per CU) and repetitions
-    const int mults[4] = {4, 8, 16, 32};
-    for (int kind = 0; kind < 4; ++kind) {
-        float best = 1e30f;
-        for (int rep = 0; rep < 4 * 4; ++rep) {
-            const int grid = ncu * mults[rep % 4];
-            if (!ok(hipEventRecord(e0), "record")) return 1;
-            if (kind == 0) k_read<<<grid, 256>>>(A, n, sink);
-            if (kind == 1) k_write<<<grid, 256>>>(A, n);
-            if (kind == 2) k_copy<<<grid, 256>>>(A, B, n);
-            if (kind == 3) k_rmw3<<<grid, 256>>>(A, B, C, n);
-            if (!ok(hipGetLastError(), "launch") || !ok(hipEventRecord(e1), "record") ||
-                !ok(hipEventSynchronize(e1), "sync"))
-                return 1;
-            float ms = 0.0f;
-            if (!ok(hipEventElapsedTime(&ms, e0, e1), "elapsed")) return 1;
-            if (rep >= 4 && ms < best) best = ms;    // the first pass over the grids warms up
-        }
-        const double moved = (kind < 2 ? 1.0 : kind == 2 ? 2.0 : 6.0) * (double)bytes;
-        gbs[kind] = moved / (best * 1e-3) / 1e9;
-    }
+    Timer tm;
+    if (!tm.init()) return 1;
+    const char *names[5] = {"read", "write", "copy", "rmw3", "rmw3_tile"};
+    Best best[5];
+    for (int kind = 0; kind < 4; ++kind)
+        if (!stream_kind<1>(kind, A, B, C, sink, n, ncu, tm, best[kind]) ||
+            !stream_kind<2>(kind, A, B, C, sink, n, ncu, tm, best[kind]) ||
+            !stream_kind<4>(kind, A, B, C, sink, n, ncu, tm, best[kind]))
+            return 1;
+    const int tiles_p = (int)(bytes / (128ull * 4096 * 2));  // 128-row tile rows per stream
+    if (!tile_kind<1>(A, B, C, tiles_p, tm, best[4]) || !tile_kind<2>(A, B, C, tiles_p, tm, best[4]) ||
+        !tile_kind<8>(A, B, C, tiles_p, tm, best[4]))
+        return 1;
     printf("{\"unit\": \"GB/s\", \"bytes_per_stream\": %zu", bytes);
-    for (int kind = 0; kind < 4; ++kind) printf(", \"%s\": %.1f", names[kind], gbs[kind]);
-    printf("}\n");
+    for (int kind = 0; kind < 5; ++kind) printf(", \"%s\": %.1f", names[kind], best[kind].gbs);
+    printf(", \"shapes\": {");
+    for (int kind = 0; kind < 5; ++kind) printf("%s\"%s\": \"%s\"", kind ? ", " : "", names[kind], best[kind].shape);
+    printf("}}\n");
     (void)hipFree(A); (void)hipFree(B); (void)hipFree(C); (void)hipFree(sink);
     return 0;
 }
