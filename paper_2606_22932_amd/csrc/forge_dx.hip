@@ -10,22 +10,24 @@
 // and up) each contribute a term to that input's gradient; one launch sums them by running
 // the GEMM's K loop over their concatenated d_out axes, with one rounding to bf16 at the end.
 //
-// One workgroup of four waves owns an output tile dX[t0 : t0+BT, q0 : q0+BQ] held in fp32
-// registers.  MFMA (v_mfma_f32_32x32x16_bf16) operand A is W^T (M = q along d_in, K = p
+// One workgroup owns an output tile dX[t0 : t0+BT, q0 : q0+BQ] held in fp32 registers: four
+// waves for 64- and 128-row tiles of 128 columns, eight waves (two per SIMD, each holding
+// 128 x 64 outputs) for 256 x 256 tiles, which halve the LDS fragment reads per flop and
+// are chosen once they alone fill the compute units.  MFMA (v_mfma_f32_32x32x16_bf16) operand A is W^T (M = q along d_in, K = p
 // along d_out), operand B is dY^T (K = p, N = t); each lane of a 32x32 result holds four
 // consecutive q of one token row, which is the order the tile is staged in for its stores.
 #include "forge_device.h"
 
 namespace forge_impl {
 
-#ifndef FORGE_DX_BT               // token rows per tile: 64, 128, or 0 to choose by shape
+#ifndef FORGE_DX_BT               // token rows per tile: 64, 128, 256, or 0 to choose by shape
 #define FORGE_DX_BT 0
 #endif
 
 constexpr int DX_NS = 4;          // LDS ring depth (chunks)
 
-constexpr int DX_NT = 256;        // threads per workgroup (four waves)
-constexpr int DX_BQ = 128;        // columns of dX per tile
+constexpr int DX_NT = 256;        // threads per workgroup of the 64- and 128-row tiles
+constexpr int DX_BQ = 128;        // their columns of dX per tile
 
 // Operand path: a ring of NS LDS stages; a stage holds one chunk of BK rows p of W
 // (columns q0 .. q0+BQ-1, row pitch 2*BQ bytes) followed by the matching BK columns of dY
@@ -40,12 +42,12 @@ constexpr int DX_BQ = 128;        // columns of dX per tile
 // ds_read_b64_tr_b16 -- lane s of each 16 points at row p0 + s/4, column c0 + 4 (s%4), so
 // that lane i receives column c0 + i, rows p0 .. p0+3; dY's (8 consecutive p of one t) are
 // one 16-byte ds_read_b128 each.
-template <int BT, int BQ, int NA, int NB, int BK, int NS>
+template <int BT, int BQ, int NA, int NB, int BK, int NS, int NW = 4>
 struct DxTile {
     static_assert(BK == 32 || BK == 64, "chunks of 32 or 64 rows of W");
     static constexpr int WQ = BQ / (32 * NA);            // waves along q (each 32*NA columns)
     static constexpr int WT = BT / (32 * NB);            // waves along t (each 32*NB rows)
-    static_assert(WQ * WT == 4, "four waves");
+    static_assert(WQ * WT == NW, "waves");
     static constexpr int WROWB = BQ * 2;                 // LDS bytes per W row
     static constexpr int YROWB = BK * 2;                 // LDS bytes per dY row
     static constexpr int PPR = BK / 8;                   // 16-byte pieces per dY row
@@ -53,14 +55,17 @@ struct DxTile {
     static_assert(WROWB >= 256, "the W swizzle assumes rows of at least 256 bytes");
     static constexpr int WCH = BK * BQ / 8;              // 16-byte pieces of W per chunk
     static constexpr int YCH = BT * BK / 8;              // 16-byte pieces of dY per chunk
-    static_assert(WCH % 256 == 0 && YCH % 256 == 0, "a wave's k-th DMA is all W or all dY");
-    static constexpr int KW = WCH / 256;                 // DMA instructions per wave for W
-    static constexpr int DPC = (WCH + YCH) / 256;        // DMA instructions per wave per chunk
+    static_assert(WCH % (64 * NW) == 0 && YCH % (64 * NW) == 0, "a wave's k-th DMA is all W or all dY");
+    static constexpr int KW = WCH / (64 * NW);           // DMA instructions per wave for W
+    static constexpr int DPC = (WCH + YCH) / (64 * NW);  // DMA instructions per wave per chunk
     static constexpr int KY = DPC - KW;
     static constexpr int STAGE_BYTES = (WCH + YCH) * 16;
     static constexpr int OP = BQ + 4;                    // fp32 pitch of the staged output tile
+    static constexpr int OPB = BQ + 8;                   // bf16 pitch of the staged output tile
+    static constexpr bool OUT_BF16 = BT * OP * 4 > 96 * 1024;   // big tiles stage rounded bf16
+    static constexpr int OUT_BYTES = OUT_BF16 ? BT * OPB * 2 : BT * OP * 4;
     static constexpr int RING = NS * STAGE_BYTES;
-    static constexpr int LDS_BYTES = RING > BT * OP * 4 ? RING : BT * OP * 4;
+    static constexpr int LDS_BYTES = RING > OUT_BYTES ? RING : OUT_BYTES;
     static constexpr int NRD = 2 * NA + NB;              // LDS reads per 16-row K step
 
     f32x16_t acc[NA][NB];
@@ -82,7 +87,7 @@ struct DxTile {
     {
 #pragma unroll
         for (int k = 0; k < KW; ++k) {
-            const int L = (k * 4 + wave) * 64 + lane;
+            const int L = (k * NW + wave) * 64 + lane;
             const int r = L / (BQ / 8);
             const int col = q0 + 8 * ((L % (BQ / 8)) ^ wswz(r));
             const uint64_t off = ((uint64_t)r * (uint64_t)g.d_in + (uint64_t)col) * 2u;
@@ -90,7 +95,7 @@ struct DxTile {
         }
 #pragma unroll
         for (int k = 0; k < KY; ++k) {
-            const int L = (k * 4 + wave) * 64 + lane;
+            const int L = (k * NW + wave) * 64 + lane;
             const int t = L / PPR;
             yr[k] = (t0 + t < g.T) ? t : -1;
             yc[k] = 8 * ((L % PPR) ^ yswz(t));
@@ -128,12 +133,12 @@ struct DxTile {
         const int rem = sg.d_out - p0;
 #pragma unroll
         for (int k = 0; k < KW; ++k) {
-            auto *dst = (__attribute__((address_space(3))) void *)(stage + (k * 4 + wave) * 1024);
+            auto *dst = (__attribute__((address_space(3))) void *)(stage + (k * NW + wave) * 1024);
             __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, dst, 16, wo[k], 0, 0, 0);
         }
 #pragma unroll
         for (int k = 0; k < KY; ++k) {
-            auto *dst = (__attribute__((address_space(3))) void *)(stage + ((KW + k) * 4 + wave) * 1024);
+            auto *dst = (__attribute__((address_space(3))) void *)(stage + ((KW + k) * NW + wave) * 1024);
             const uint32_t off = (yr[k] >= 0 && yc[k] < rem)
                                      ? ((uint32_t)yr[k] * (uint32_t)sg.d_out + (uint32_t)yc[k]) * 2u
                                      : OOR_OFFSET;
@@ -171,6 +176,11 @@ struct DxTile {
         }
 #pragma unroll
         for (int j = 0; j < NB; ++j) read128(fb[0][j], st + tb[j][2 * H]);
+        // at most 15 LDS reads outstanding (lgkmcnt's range): with many fragments per
+        // step the second step's reads follow the first step's wait
+        constexpr bool ALL_AHEAD = 2 * NRD <= 15;
+        static_assert(NRD <= 15, "lgkmcnt range");
+        if constexpr (!ALL_AHEAD) wait_lgkm<0>(fa[0], fb[0]);
 #pragma unroll
         for (int i = 0; i < NA; ++i) {
             tr_read<R + 16 * WROWB>(fa[1][i][0], st + ta[i]);
@@ -178,7 +188,7 @@ struct DxTile {
         }
 #pragma unroll
         for (int j = 0; j < NB; ++j) read128(fb[1][j], st + tb[j][2 * H + 1]);
-        wait_lgkm<NRD>(fa[0], fb[0]);
+        if constexpr (ALL_AHEAD) wait_lgkm<NRD>(fa[0], fb[0]);
 #pragma unroll
         for (int i = 0; i < NA; ++i)
 #pragma unroll
@@ -272,6 +282,10 @@ struct DxTile {
     __device__ __forceinline__ void store(const DxArgs &g, int t0, int q0, unsigned char *lds, int wave,
                                           int lane, int tid) const
     {
+        if constexpr (OUT_BF16) {
+            store_bf16(g, t0, q0, lds, wave, lane, tid);
+            return;
+        }
         float *Os = reinterpret_cast<float *>(lds);
         const int wq = wave % WQ, wt = wave / WQ;
 #pragma unroll
@@ -288,7 +302,7 @@ struct DxTile {
                 }
             }
         lds_barrier();
-        constexpr int LPR = BQ / 8, RPP = DX_NT / LPR;
+        constexpr int LPR = BQ / 8, RPP = 64 * NW / LPR;
         const int rs = tid / LPR, qo = (tid % LPR) * 8, q = q0 + qo;
         if (q >= g.d_in) return;
 #pragma unroll
@@ -303,33 +317,72 @@ struct DxTile {
             *reinterpret_cast<u32x4_t *>(g.dX + (size_t)(t0 + t) * (size_t)g.d_in + q) = w;
         }
     }
+
+    // Big tiles: each accumulator rounded to bf16 (round to nearest even) in registers, the
+    // tile staged as bf16, then 16-byte stores of whole rows.  Rounding before or after the
+    // staging gives the same bits.
+    __device__ __forceinline__ void store_bf16(const DxArgs &g, int t0, int q0, unsigned char *lds, int wave,
+                                               int lane, int tid) const
+    {
+        uint16_t *Ob = reinterpret_cast<uint16_t *>(lds);
+        const int wq = wave % WQ, wt = wave / WQ;
+#pragma unroll
+        for (int i = 0; i < NA; ++i)
+#pragma unroll
+            for (int j = 0; j < NB; ++j) {
+                const int t = wt * 32 * NB + j * 32 + (lane & 31);
+#pragma unroll
+                for (int q4 = 0; q4 < 4; ++q4) {
+                    const int q = wq * 32 * NA + i * 32 + q4 * 8 + (lane >> 5) * 4;
+                    const u32x2_t v = {pack_bf16(acc[i][j][4 * q4], acc[i][j][4 * q4 + 1]),
+                                       pack_bf16(acc[i][j][4 * q4 + 2], acc[i][j][4 * q4 + 3])};
+                    *reinterpret_cast<u32x2_t *>(Ob + t * OPB + q) = v;
+                }
+            }
+        lds_barrier();
+        constexpr int LPR = BQ / 8, RPP = 64 * NW / LPR;
+        const int rs = tid / LPR, qo = (tid % LPR) * 8, q = q0 + qo;
+        if (q >= g.d_in) return;
+#pragma unroll
+        for (int r = 0; r < BT; r += RPP) {
+            const int t = r + rs;
+            if (t0 + t >= g.T) break;
+            const u32x4_t w = *reinterpret_cast<const u32x4_t *>(Ob + t * OPB + qo);
+            *reinterpret_cast<u32x4_t *>(g.dX + (size_t)(t0 + t) * (size_t)g.d_in + q) = w;
+        }
+    }
 };
 
 // 128-row tiles use 32-row chunks (66 KB of LDS: two workgroups per CU); 64-row tiles,
 // which run one workgroup per CU on the short token axes they are chosen for, use 64-row
 // chunks (96 KB), which halves the barriers per K and keeps twice the bytes in flight.
-template <int BT, int NA, int NB, int BK, int NS>
-__global__ void __launch_bounds__(DX_NT, BK == 64 ? 1 : 2) dx_kernel(DxArgs g)
+// 256 x 256 tiles: eight waves, 32-row chunks (128 KB ring), output staged as bf16 (132 KB),
+// one workgroup per CU.
+template <int BT, int NA, int NB, int BK, int NS, int BQ = DX_BQ, int NW = 4>
+__global__ void __launch_bounds__(64 * NW, (BK == 64 || NW > 4) ? 1 : 2) dx_kernel(DxArgs g)
 {
-    using L = DxTile<BT, DX_BQ, NA, NB, BK, NS>;
+    using L = DxTile<BT, BQ, NA, NB, BK, NS, NW>;
     __shared__ __attribute__((aligned(16))) unsigned char smem[L::LDS_BYTES];
     const int tid = threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int lane = tid & 63;
     int tt, tq;
     tile_of(blockIdx.x, gridDim.x, g.tiles_t, g.tiles_q, g.group_t, tt, tq);
-    const int t0 = tt * BT, q0 = tq * DX_BQ;
+    const int t0 = tt * BT, q0 = tq * BQ;
     L tile;
     tile.run(g, t0, q0, smem, wave, lane);
     tile.store(g, t0, q0, smem, wave, lane, tid);
 }
 
-// Token rows per tile: 128 (2x2 waves of 64x64) once the 128x128 tiles alone cover every
-// compute unit, else 64 (4x1 waves of 32 columns x 64 rows), which doubles the tile count
-// for the short token axes of fine-tuning-sized batches.
+// Token rows per tile: 256 (256 x 256 tiles, 2x4 waves of 128x64) once those alone cover
+// every compute unit; else 128 (2x2 waves of 64x64) once the 128x128 tiles do; else 64 (4x1
+// waves of 32 columns x 64 rows), which doubles the tile count for the short token axes of
+// fine-tuning-sized batches.  Every choice sums over K in the same order: dX is the same
+// bits whichever tile computes it.
 static int dx_rows(int T, int d_in)
 {
     if (FORGE_DX_BT) return FORGE_DX_BT;
+    if ((long)((T + 255) / 256) * (long)((d_in + 255) / 256) >= (long)device_cu_count()) return 256;
     const long t128 = (long)((T + 127) / 128) * (long)((d_in + DX_BQ - 1) / DX_BQ);
     return t128 >= (long)device_cu_count() ? 128 : 64;
 }
@@ -342,16 +395,19 @@ hipError_t launch_dx(const DxSeg *s, int n, uint16_t *dX, int T, int d_in, hipSt
     g.nch = 0;
     for (int i = 0; i < MAX_GROUP; ++i) g.s[i] = i < n ? s[i] : DxSeg{nullptr, nullptr, 0};
     const int bt = dx_rows(T, d_in);
-    const int bk = bt == 128 ? 32 : 64;
+    const int bk = bt == 64 ? 64 : 32;
     for (int i = 0; i < n; ++i) g.nch += (s[i].d_out + bk - 1) / bk;
     g.dX = dX;
     g.T = T;
     g.d_in = d_in;
+    const int bq = bt == 256 ? 256 : DX_BQ;
     g.tiles_t = (T + bt - 1) / bt;
-    g.tiles_q = (d_in + DX_BQ - 1) / DX_BQ;
+    g.tiles_q = (d_in + bq - 1) / bq;
     g.group_t = g.tiles_t < 16 ? g.tiles_t : 16;
     const int ntiles = g.tiles_t * g.tiles_q;
-    if (bt == 128)
+    if (bt == 256)
+        hipLaunchKernelGGL((dx_kernel<256, 4, 2, 32, DX_NS, 256, 8>), dim3(ntiles), dim3(512), 0, st, g);
+    else if (bt == 128)
         hipLaunchKernelGGL((dx_kernel<128, 2, 2, 32, DX_NS>), dim3(ntiles), dim3(DX_NT), 0, st, g);
     else
         hipLaunchKernelGGL((dx_kernel<64, 1, 2, 64, DX_NS>), dim3(ntiles), dim3(DX_NT), 0, st, g);

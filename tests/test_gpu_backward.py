@@ -1,8 +1,9 @@
 """GPU parity of the layer-level backward: dX = dY W from the pre-update W, then the fused step.
 
-* ``forge_input_grad`` against the oracle's fp64 dX on ragged and multi-tile shapes, both
-  tile heights (64 and 128 token rows), and the masking of the K tail (a chunk past a
-  segment's d_out must read zeros, not the next dY row or memory past W);
+* ``forge_input_grad`` against the oracle's fp64 dX on ragged and multi-tile shapes, all
+  three tile shapes (64 and 128 token rows by 128 columns, and 256 x 256 with eight waves),
+  and the masking of the K tail (a chunk past a segment's d_out must read zeros, not the
+  next dY row or memory past W);
 * ``forge_linear_backward`` equals ``forge_input_grad`` on the pre-update W followed by
   ``forge_linear_step``, bit for bit, and matches the oracle;
 * ``forge_linear_backward_grouped`` sums the projections of one input (q, k, v) into one
@@ -53,9 +54,11 @@ def _rand(shape, std, seed):
 
 
 # (T, d_in, d_out): multi-tile, ragged in every axis, a lone token row, the 128-row tiles
-# (4096 x 2048 gives 512 tiles of 128 x 128, two per compute unit), and a single 8-wide tile.
+# (4096 x 2048 gives 512 tiles of 128 x 128, two per compute unit), a single 8-wide tile,
+# and the 256 x 256 tiles (16 x 16 and 17 x 17 of them, ragged on both axes and, with
+# d_out = 1032, in the last K chunk).
 DX_SHAPES = [(128, 256, 256), (200, 136, 40), (1000, 520, 776), (1, 128, 4096), (4096, 2048, 264),
-             (64, 8, 8), (77, 1032, 1000)]
+             (64, 8, 8), (77, 1032, 1000), (4000, 4040, 200), (4100, 4104, 1032)]
 
 
 @pytest.mark.parametrize("shape", DX_SHAPES, ids=lambda s: "x".join(map(str, s)))
