@@ -1627,7 +1627,9 @@ static hipError_t launch_group(const Args *a, int n, hipStream_t st)
     g.start[0] = 0;
     for (int i = 0; i < n; ++i) {
         int nt;
-        g.a[i] = with_grid(a[i], BP, BQ, nt);
+        // int8 row-block state: groups of 8 tile rows (measured on the MLP projections at
+        // T = 512: 5 % faster than the shape rule, whose 24-row groups suit bf16 state)
+        g.a[i] = with_grid(a[i], BP, BQ, nt, MK == MK_I8R64 ? 8 : 0);
         g.start[i + 1] = g.start[i] + nt;
     }
     for (int i = n; i < MAX_GROUP; ++i) {
