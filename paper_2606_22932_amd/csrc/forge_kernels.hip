@@ -462,6 +462,21 @@ template <> struct Rule<EPI_MUON> {           // B' = mu B + G (the GEMM's beta)
 // The epilogue of a rule on fp32 or bf16 state.  The stream waves prefetch the tile's
 // bf16 W and state into registers while the mainloop runs (fp32 state would not fit and
 // is loaded here); then each lane updates 8 consecutive columns of one row per pass.
+// Byte offset of element (p, q) of a [rows, ld] tensor with `eb`-byte elements, or an
+// offset past every buffer end (reads zero) when the element lies outside the tensor.
+__device__ __forceinline__ uint32_t elem_off(int p, int q, int rows, int ld, int eb)
+{
+    if (p >= rows || q >= ld) return OOR_OFFSET;
+    const uint64_t off = ((uint64_t)p * (uint64_t)ld + (uint64_t)q) * (uint64_t)eb;
+    return off < OOR_OFFSET ? (uint32_t)off : OOR_OFFSET;
+}
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_of(const void *base, uint64_t bytes)
+{
+    const uint32_t n = bytes < OOR_OFFSET ? (uint32_t)bytes : OOR_OFFSET;
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)n, 0x00020000);
+}
+
 template <int BP, int BQ, int MK, int E>
 struct EpiRule {
     using M = EpiMap<BP, BQ>;
@@ -480,18 +495,14 @@ struct EpiRule {
     __device__ __forceinline__ void prefetch_pass(const Args &a, int p0, int q0, int s)
     {
         if constexpr (PREFETCH) {
+            // buffer loads: elements outside the matrix read as zero
             const int rs = s / M::LPR, q = q0 + (s % M::LPR) * 8;
             const int p = p0 + I * M::RPP + rs;
-            const u32x4_t z = {0u, 0u, 0u, 0u};
-            if constexpr (R::W_RW) pw[I] = z;
-            if constexpr (R::NS >= 1) ps1[I] = z;
-            if constexpr (R::NS >= 2) ps2[I] = z;
-            if (q < a.d_in && p < a.d_out) {
-                const size_t off = (size_t)p * a.d_in + q;
-                if constexpr (R::W_RW) pw[I] = ld_nt<u32x4_t>(a.W + off);
-                if constexpr (R::NS >= 1) ps1[I] = ld_nt<u32x4_t>(static_cast<const uint16_t *>(a.m) + off);
-                if constexpr (R::NS >= 2) ps2[I] = ld_nt<u32x4_t>(static_cast<const uint16_t *>(a.v) + off);
-            }
+            const uint64_t n = 2ull * (uint64_t)a.d_out * (uint64_t)a.d_in;
+            const uint32_t off = elem_off(p, q, a.d_out, a.d_in, 2);
+            if constexpr (R::W_RW) pw[I] = __builtin_amdgcn_raw_buffer_load_b128(rsrc_of(a.W, n), off, 0, 2);
+            if constexpr (R::NS >= 1) ps1[I] = __builtin_amdgcn_raw_buffer_load_b128(rsrc_of(a.m, n), off, 0, 2);
+            if constexpr (R::NS >= 2) ps2[I] = __builtin_amdgcn_raw_buffer_load_b128(rsrc_of(a.v, n), off, 0, 2);
         }
     }
 
@@ -599,10 +610,64 @@ struct EpiRule {
 template <int BP, int BQ, int MK>
 using EpiAdamW = EpiRule<BP, BQ, MK, EPI_ADAMW>;
 
+// The absmax reductions below run on the bit patterns of non-negative floats (+0 and up),
+// whose signed-integer order is their numeric order.
+//
+// Lane exchange within a row of 16 lanes (DPP; no LDS round trip).  CTRL is a DPP control:
+// 0xB1 and 0x4E are the quad permutations [1,0,3,2] and [2,3,0,1], 0x141 mirrors each half
+// row of 8 lanes, 0x128 rotates the row by 8.
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int x)
+{
+    return __builtin_amdgcn_mov_dpp(x, CTRL, 0xF, 0xF, true);
+}
+
+// Max of x >= 0 over each aligned group of 8 lanes, returned to all 8 (every lane active).
+__device__ __forceinline__ float max8(float x)
+{
+    int b = __float_as_int(x);
+    b = max(b, dpp_i<0xB1>(b));
+    b = max(b, dpp_i<0x4E>(b));
+    return __int_as_float(max(b, dpp_i<0x141>(b)));
+}
+
+// int8 codes of eight values y = x / s: clamped to [lo, 127] (lo = -127 for m; for sqrt(v)
+// or v, 1 in a non-zero block and 0 in an all-zero one), rounded to nearest even, packed.
+// Clamping before rounding gives the same integer, as both bounds are integers.  Adding
+// 1.5 * 2^23 does the rounding (the sum's ulp is 1) and leaves the integer's two's-
+// complement low byte as the sum's low byte.
+__device__ __forceinline__ u32x2_t pack_codes(const float (&y)[8], const float (&lo)[8])
+{
+    uint32_t b[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) b[e] = __float_as_uint(__builtin_amdgcn_fmed3f(y[e], lo[e], 127.0f) + 12582912.0f);
+    u32x2_t r;
+#pragma unroll
+    for (int k = 0; k < 2; ++k)
+        r[k] = __builtin_amdgcn_perm(b[4 * k + 1], b[4 * k], 0x0c0c0400u) |
+               __builtin_amdgcn_perm(b[4 * k + 3], b[4 * k + 2], 0x04000c0cu);
+    return r;
+}
+__device__ __forceinline__ u32x2_t pack_codes(const float (&y)[8], float lo)
+{
+    const float l[8] = {lo, lo, lo, lo, lo, lo, lo, lo};
+    return pack_codes(y, l);
+}
+
+// x / 127 in fp32, correctly rounded for every finite x >= 0: the product with RN(1/127)
+// and one fma correction from its exact remainder.  Checked against IEEE division over
+// every non-negative finite float.
+__device__ __forceinline__ float div127(float x)
+{
+    constexpr float R = 1.0f / 127.0f;
+    const float q = x * R;
+    return __builtin_fmaf(__builtin_fmaf(-q, 127.0f, x), R, q);
+}
+
 // AdamW on int8 moments in the 64-wide row-block layout of App. B: one fp32 scale per 64
 // consecutive elements of a row, m = s_m q_m and v = s_v q_v (v stored itself).  A block is
 // exactly the 8 consecutive lanes that hold its row's 64 columns in one pass, so the new
-// block absmax closes with three xor shuffles and each row is dequantised, updated and
+// block absmax closes with three DPP exchanges and each row is dequantised, updated and
 // re-quantised in a single pass: s = absmax / 127 (fp32, correctly rounded),
 // q = round_half_even(x / s) clamped to [-127, 127], v codes at least 1 in a non-zero block.
 // The weight update reads the unquantised fp32 m', v'.
@@ -619,20 +684,17 @@ struct EpiI8Row {
     template <int I>
     __device__ __forceinline__ void prefetch_pass(const Args &a, int p0, int q0, int s)
     {
+        // buffer loads: elements outside the matrix read as zero
         const int rs = s / M::LPR, q = q0 + (s % M::LPR) * 8;
-        const int p = p0 + I * M::RPP + rs;
-        pw[I] = u32x4_t{0u, 0u, 0u, 0u};
-        pm[I] = pv[I] = u32x2_t{0u, 0u};
-        sm[I] = sv[I] = 0.0f;
-        if (q < a.d_in && p < a.d_out) {
-            const size_t off = (size_t)p * a.d_in + q;
-            const size_t so = (size_t)p * nblocks(a) + q / I8_ROW_BLOCK;
-            pw[I] = ld_nt<u32x4_t>(a.W + off);
-            pm[I] = ld_nt<u32x2_t>(static_cast<const int8_t *>(a.m) + off);
-            pv[I] = ld_nt<u32x2_t>(static_cast<const int8_t *>(a.v) + off);
-            sm[I] = a.ms[so];
-            sv[I] = a.vs[so];
-        }
+        const int p = p0 + I * M::RPP + rs, nb = nblocks(a);
+        const uint64_t n = (uint64_t)a.d_out * (uint64_t)a.d_in, ns = 4ull * (uint64_t)a.d_out * (uint64_t)nb;
+        const uint32_t off = elem_off(p, q, a.d_out, a.d_in, 1);
+        const uint32_t so = q < a.d_in ? elem_off(p, q / I8_ROW_BLOCK, a.d_out, nb, 4) : OOR_OFFSET;
+        pw[I] = __builtin_amdgcn_raw_buffer_load_b128(rsrc_of(a.W, 2ull * n), off == OOR_OFFSET ? off : 2u * off, 0, 2);
+        pm[I] = __builtin_amdgcn_raw_buffer_load_b64(rsrc_of(a.m, n), off, 0, 2);
+        pv[I] = __builtin_amdgcn_raw_buffer_load_b64(rsrc_of(a.v, n), off, 0, 2);
+        sm[I] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rsrc_of(a.ms, ns), so, 0, 0));
+        sv[I] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rsrc_of(a.vs, ns), so, 0, 0));
     }
 
     template <int I = 0>
@@ -670,31 +732,26 @@ struct EpiI8Row {
                 av = fmaxf(av, vo[e]);
             }
             if (!ok) am = av = 0.0f;
-#pragma unroll
-            for (int d = 1; d < 8; d <<= 1) {
-                am = fmaxf(am, __shfl_xor(am, d));
-                av = fmaxf(av, __shfl_xor(av, d));
-            }
-            const float scm = am / 127.0f, scv = av / 127.0f;
+            am = max8(am);
+            av = max8(av);
+            const float scm = div127(am), scv = div127(av);
             const float rcm = scm > 0.0f ? __builtin_amdgcn_rcpf(scm) : 0.0f;
             const float rcv = scv > 0.0f ? __builtin_amdgcn_rcpf(scv) : 0.0f;
-            uint32_t cm[2] = {0u, 0u}, cv[2] = {0u, 0u};
+            float ym[8], yv[8];
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                const float qm = fminf(fmaxf(__builtin_rintf(mo[e] * rcm), -127.0f), 127.0f);
-                float qv = fminf(fmaxf(__builtin_rintf(vo[e] * rcv), 1.0f), 127.0f);
-                if (!(rcv > 0.0f)) qv = 0.0f;
-                cm[e >> 2] |= ((uint32_t)(int32_t)qm & 0xFFu) << (8 * (e & 3));
-                cv[e >> 2] |= ((uint32_t)(int32_t)qv & 0xFFu) << (8 * (e & 3));
+                ym[e] = mo[e] * rcm;
+                yv[e] = vo[e] * rcv;
             }
+            const u32x2_t cm = pack_codes(ym, -127.0f), cv = pack_codes(yv, rcv > 0.0f ? 1.0f : 0.0f);
             if (ok) {
                 const size_t off = (size_t)p * a.d_in + q;
                 u32x4_t wn;
 #pragma unroll
                 for (int k = 0; k < 4; ++k) wn[k] = pack_bf16(wo[2 * k], wo[2 * k + 1]);
                 st_nt<u32x4_t>(a.W + off, wn);
-                st_nt<u32x2_t>(static_cast<int8_t *>(a.m) + off, u32x2_t{cm[0], cm[1]});
-                st_nt<u32x2_t>(static_cast<int8_t *>(a.v) + off, u32x2_t{cv[0], cv[1]});
+                st_nt<u32x2_t>(static_cast<int8_t *>(a.m) + off, cm);
+                st_nt<u32x2_t>(static_cast<int8_t *>(a.v) + off, cv);
                 if ((s & 7) == 0) {
                     const size_t so = (size_t)p * nblocks(a) + q / I8_ROW_BLOCK;
                     a.ms[so] = scm;
@@ -1228,21 +1285,6 @@ __global__ void __launch_bounds__(NROLE, 2) adamw_kernel(Args a)
 // pass 2.  Every workgroup barrier is executed by all waves: a period has nb = max(nch, 2)
 // barriers (the mainloop's chunk barriers, padded), then H1 and H2.
 
-// Byte offset of element (p, q) of a [rows, ld] tensor with `eb`-byte elements, or an
-// offset past every buffer end (reads zero) when the element lies outside the tensor.
-__device__ __forceinline__ uint32_t elem_off(int p, int q, int rows, int ld, int eb)
-{
-    if (p >= rows || q >= ld) return OOR_OFFSET;
-    const uint64_t off = ((uint64_t)p * (uint64_t)ld + (uint64_t)q) * (uint64_t)eb;
-    return off < OOR_OFFSET ? (uint32_t)off : OOR_OFFSET;
-}
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_of(const void *base, uint64_t bytes)
-{
-    const uint32_t n = bytes < OOR_OFFSET ? (uint32_t)bytes : OOR_OFFSET;
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)n, 0x00020000);
-}
-
 template <int NSW>
 struct StreamI8 {
     using M = EpiMap<BP_I8, BQ_I8, NSW * 64>;           // 8 lanes per row, 8*NSW rows per pass
@@ -1253,6 +1295,7 @@ struct StreamI8 {
     float am[8], av[8];                                 // absmax partials
     float rv[NPASS][8];                                 // sqrt(v') of each pass, for pass 2
     float rcm[8], rcv[8];                               // reciprocals of the new scales
+    float lov[8];                                       // least sqrt(v) code: 1, or 0 in an all-zero block
 
     // Loads of the state of tile (p0, q0) of matrix a: row I of every pass, then the scales.
     template <int I>
@@ -1385,6 +1428,20 @@ struct StreamI8 {
         }
     }
 
+    // Max of x >= 0 over the 8 lanes l, l^8, ..., l^56 that hold the same columns (a wave's 8 rows):
+    // a DPP rotation by 8 within each row of 16 lanes, then the CDNA4 lane swaps of rows
+    // 2k with 2k+1 and of the two halves of the wave.
+    static __device__ __forceinline__ float max_rows(float x)
+    {
+        static_assert(M::LPR == 8, "8 lanes per row");
+        int b = __float_as_int(x);
+        b = max(b, dpp_i<0x128>(b));
+        const auto h = __builtin_amdgcn_permlane16_swap(b, b, false, false);
+        b = max((int)h[0], (int)h[1]);
+        const auto w = __builtin_amdgcn_permlane32_swap(b, b, false, false);
+        return __int_as_float(max((int)w[0], (int)w[1]));
+    }
+
     // Block absmax of this lane's columns over its rows: within the wave, then (through
     // LDS, across the barrier that follows) across the NSW stream waves.
     __device__ __forceinline__ void partials(int s, float *red)
@@ -1392,11 +1449,8 @@ struct StreamI8 {
         const int qo = (s % M::LPR) * 8;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-#pragma unroll
-            for (int d = M::LPR; d < 64; d <<= 1) {
-                am[e] = fmaxf(am[e], __shfl_xor(am[e], d));
-                av[e] = fmaxf(av[e], __shfl_xor(av[e], d));
-            }
+            am[e] = max_rows(am[e]);
+            av[e] = max_rows(av[e]);
         }
         const int sw = s >> 6;
         if ((s & 63) < M::LPR) {
@@ -1441,6 +1495,8 @@ struct StreamI8 {
             rcm[e] = m0[e]; rcm[e + 4] = m1[e];
             rcv[e] = v0[e]; rcv[e + 4] = v1[e];
         }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) lov[e] = rcv[e] > 0.0f ? 1.0f : 0.0f;
     }
 
     // Pass 2, row I: m' (from the LDS stage) and sqrt(v') (from registers) quantised
@@ -1449,21 +1505,18 @@ struct StreamI8 {
     __device__ __forceinline__ void pass2(const Args &a, int p0, int q0, int s, const float *Gs)
     {
         const int p = p0 + I * M::RPP + s / M::LPR, q = q0 + (s % M::LPR) * 8;
-        uint32_t qm2[2] = {0u, 0u}, qv2[2] = {0u, 0u};
-        float mo[8];
-        g_row<I>(Gs, s, mo);
+        float ym[8], yv[8];
+        g_row<I>(Gs, s, ym);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-            const float qm = fminf(fmaxf(__builtin_rintf(mo[e] * rcm[e]), -127.0f), 127.0f);
-            float qv = fminf(fmaxf(__builtin_rintf(rv[I][e] * rcv[e]), 1.0f), 127.0f);
-            if (!(rcv[e] > 0.0f)) qv = 0.0f;
-            qm2[e >> 2] |= ((uint32_t)(int32_t)qm & 0xFFu) << (8 * (e & 3));
-            qv2[e >> 2] |= ((uint32_t)(int32_t)qv & 0xFFu) << (8 * (e & 3));
+            ym[e] *= rcm[e];
+            yv[e] = rv[I][e] * rcv[e];
         }
+        const u32x2_t qm = pack_codes(ym, -127.0f), qv = pack_codes(yv, lov);
         if (p < a.d_out && q < a.d_in) {
             const size_t off = (size_t)p * a.d_in + q;
-            st_nt<u32x2_t>(static_cast<int8_t *>(a.m) + off, u32x2_t{qm2[0], qm2[1]});
-            st_nt<u32x2_t>(static_cast<int8_t *>(a.v) + off, u32x2_t{qv2[0], qv2[1]});
+            st_nt<u32x2_t>(static_cast<int8_t *>(a.m) + off, qm);
+            st_nt<u32x2_t>(static_cast<int8_t *>(a.v) + off, qv);
         }
     }
 
