@@ -34,28 +34,28 @@ COPY_BYTES = 1 << 30           # size of the calibration copy (--copy-calibratio
 # sources whose sha256 is recorded: after any change to them the figure is reported as null.
 TRAFFIC = {
     "sweep": {
-        "source_sha256": "e6229e291fb4e3c5829205beb1ddd4c5b60fdb7b00bef1b936a84e88bc68ae13",
-        "fetch_kib_per_launch": 207371.7,     # FETCH_SIZE, mean over the 129 launches of a step
-        "write_kib_per_launch": 340895.1,     # WRITE_SIZE
+        "source_sha256": "2b76028b052c44212bbda669438c71bb741e59c0c7b53931571d553560e08d57",
+        "fetch_kib_per_launch": 206170.3,     # FETCH_SIZE, mean over the 129 launches of a step
+        "write_kib_per_launch": 340875.9,     # WRITE_SIZE
         "fetch_scale": 1.99995,               # 1 GiB copy: FETCH_SIZE reads 524302 KiB
         "write_scale": 1.0,                   # 1 GiB copy: WRITE_SIZE reads 1048576 KiB
-        "bytes_per_launch": 773762284,        # (fetch * fetch_scale + write * write_scale) KiB
+        "bytes_per_launch": 771282175,        # (fetch * fetch_scale + write * write_scale) KiB
     },
     "mlp_i8": {
-        "source_sha256": "e6229e291fb4e3c5829205beb1ddd4c5b60fdb7b00bef1b936a84e88bc68ae13",
-        "fetch_kib_per_launch": 169131.1,     # mean over the 3 launches (gate, up, down)
-        "write_kib_per_launch": 256529.8,
+        "source_sha256": "2b76028b052c44212bbda669438c71bb741e59c0c7b53931571d553560e08d57",
+        "fetch_kib_per_launch": 169535.5,     # mean over the 3 launches (gate, up, down)
+        "write_kib_per_launch": 252100.6,
         "fetch_scale": 1.99995,
         "write_scale": 1.0,
-        "bytes_per_launch": 609057551,
+        "bytes_per_launch": 605350295,
     },
     "mlp_i8r64": {
-        "source_sha256": "e6229e291fb4e3c5829205beb1ddd4c5b60fdb7b00bef1b936a84e88bc68ae13",
-        "fetch_kib_per_launch": 155850.9,     # mean over the 3 launches (gate, up, down)
-        "write_kib_per_launch": 239073.6,
+        "source_sha256": "2b76028b052c44212bbda669438c71bb741e59c0c7b53931571d553560e08d57",
+        "fetch_kib_per_launch": 155877.2,     # mean over the 3 launches (gate, up, down)
+        "write_kib_per_launch": 239736.2,
         "fetch_scale": 1.99995,
         "write_scale": 1.0,
-        "bytes_per_launch": 563985262,
+        "bytes_per_launch": 564717741,
     },
 }
 
