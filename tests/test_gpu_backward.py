@@ -55,10 +55,13 @@ def _rand(shape, std, seed):
 
 # (T, d_in, d_out): multi-tile, ragged in every axis, a lone token row, the 128-row tiles
 # (4096 x 2048 gives 512 tiles of 128 x 128, two per compute unit), a single 8-wide tile,
-# and the 256 x 256 tiles (16 x 16 and 17 x 17 of them, ragged on both axes and, with
-# d_out = 1032, in the last K chunk).
+# 128-row tiles again at the sizes just below the 256 x 256 grid (16 x 32 of them, and 17 x 32
+# ragged on both axes), and the 256 x 256 tiles (16 x 16 and 17 x 17 of them, ragged on both
+# axes and, with d_out = 1032, in the last K chunk).  On a 256-CU device each shape past the
+# first few selects the tile named.
 DX_SHAPES = [(128, 256, 256), (200, 136, 40), (1000, 520, 776), (1, 128, 4096), (4096, 2048, 264),
-             (64, 8, 8), (77, 1032, 1000), (4000, 4040, 200), (4100, 4104, 1032)]
+             (64, 8, 8), (77, 1032, 1000), (2048, 4096, 264), (2100, 4040, 200), (4000, 4040, 200),
+             (4100, 4104, 1032)]
 
 
 @pytest.mark.parametrize("shape", DX_SHAPES, ids=lambda s: "x".join(map(str, s)))
