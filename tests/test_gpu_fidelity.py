@@ -30,8 +30,8 @@ arm's, because the standard arm rounds every gradient to bf16 before the moments
 control matches the fused arm.  Inputs: X ~ N(0, 1), dY ~ N(0, 1e-3) per step,
 W0 ~ N(0, 0.02), cold moments, AdamW lr 1e-3, betas (0.9, 0.999), eps 1e-8, wd 0.1.
 
-Run with -s to see the table (it is also written to gpurun_out/fidelity_app_e.json when
-that folder exists).
+Run with -s to see the table (it is also written as fidelity_app_e.json into the directory
+that FORGE_RESULTS_DIR names, when that is set).
 """
 import json
 import os
@@ -191,8 +191,9 @@ def test_fidelity_twenty_steps():
         vs_unrounded=metrics64(oracle.bf16_bits_to_f64(oracle.f64_to_bf16_bits(Wr)), Wr))
     out = dict(V=V, H=H, BT=BT, steps=STEPS, hyper=HP, arms=table)
     _say(json.dumps(out, indent=1))
-    if os.path.isdir("gpurun_out"):
-        with open("gpurun_out/fidelity_app_e.json", "w") as f:
+    results_dir = os.environ.get("FORGE_RESULTS_DIR")
+    if results_dir and os.path.isdir(results_dir):
+        with open(os.path.join(results_dir, "fidelity_app_e.json"), "w") as f:
             json.dump(out, f, indent=1)
 
     u = lambda k: table[k]["vs_unrounded"]["rms_rel"]
