@@ -196,8 +196,8 @@ def adamw(G, W, m, v, *, moment_dtype, lr, beta1, beta2, eps, weight_decay, step
     """One AdamW step (Algorithm 1) on an fp64 gradient; inputs are not modified.
 
     W: bf16 bits [d_out, d_in].  m, v: float32 / bf16 bits / int8 codes per ``moment_dtype``.
-    Returns a dict with the rounded new state (W, m, v, m_scale, v_scale) and the unrounded
-    fp64 values W64, m64, v64 (and the int8 quotients qm, qv when asked).
+    Returns a dict with the rounded new state (W, m, v, m_scale, v_scale), the unrounded
+    fp64 values W64, m64, v64 (and the int8 quotients qm, qv when asked) and the step.
     """
     G = _c(G, np.float64)
     d_out, d_in = G.shape
@@ -223,7 +223,7 @@ def adamw(G, W, m, v, *, moment_dtype, lr, beta1, beta2, eps, weight_decay, step
         _ptr(G), _ptr(W), _ptr(m), _ptr(v), _ptr(m_scale), _ptr(v_scale), d_in, d_out,
         int(moment_dtype), float(lr), float(beta1), float(beta2), float(eps), float(weight_decay),
         int(step), int(bool(round_grad_to_bf16)), _ptr(W64), _ptr(m64), _ptr(v64), _ptr(qm), _ptr(qv))
-    out = dict(W=W, m=m, v=v, m_scale=m_scale, v_scale=v_scale, W64=W64, m64=m64, v64=v64)
+    out = dict(W=W, m=m, v=v, m_scale=m_scale, v_scale=v_scale, W64=W64, m64=m64, v64=v64, step=int(step))
     if qm is not None:
         out.update(qm=qm, qv=qv)
     return out
@@ -279,7 +279,7 @@ def _adamw_i8row(G, W, m, v, m_scale, v_scale, *, lr, beta1, beta2, eps, weight_
     _load().forge_oracle_adamw_i8row(_ptr(G), _ptr(W), _ptr(m), _ptr(v), _ptr(m_scale), _ptr(v_scale), d_in, d_out,
                                      float(lr), float(beta1), float(beta2), float(eps), float(weight_decay), int(step),
                                      _ptr(W64), _ptr(m64), _ptr(v64), _ptr(qm), _ptr(qv))
-    out = dict(W=W, m=m, v=v, m_scale=m_scale, v_scale=v_scale, W64=W64, m64=m64, v64=v64)
+    out = dict(W=W, m=m, v=v, m_scale=m_scale, v_scale=v_scale, W64=W64, m64=m64, v64=v64, step=int(step))
     if qm is not None:
         out.update(qm=qm, qv=qv)
     return out

@@ -669,7 +669,8 @@ __device__ __forceinline__ float div127(float x)
 // exactly the 8 consecutive lanes that hold its row's 64 columns in one pass, so the new
 // block absmax closes with three DPP exchanges and each row is dequantised, updated and
 // re-quantised in a single pass: s = absmax / 127 (fp32, correctly rounded),
-// q = round_half_even(x / s) clamped to [-127, 127], v codes at least 1 in a non-zero block.
+// q = round_half_even(x * RN(1/s)) (the fp32 reciprocal of the scale, not a division)
+// clamped to [-127, 127], v codes at least 1 in a non-zero block.
 // The weight update reads the unquantised fp32 m', v'.
 template <int BP, int BQ>
 struct EpiI8Row {

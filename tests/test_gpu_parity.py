@@ -268,3 +268,42 @@ def test_int8_fused_equals_unfused_fp32_gradient_bitwise(shape):
     b = run_gpu(p, 100, path="unfused", grad="f32")
     for k in ("W", "m", "v", "m_scale", "v_scale"):
         assert np.array_equal(a[k].view(np.uint8), b[k].view(np.uint8)), k
+
+
+# Exact half-integers through the kernel's int8 quantiser (App. B's "round", read as round
+# half to even): beta1 = beta2 = 0 makes m' = G exactly, and one token with a unit input
+# side puts the values below into one int8 block whose absmax is 127, so its scale is 1
+# and every quotient is its value.
+TIE_VALUES = [127.0, 0.5, 1.5, 2.5, 3.5, -0.5, -1.5, -2.5, -3.5, 126.5, -126.5, 4.5, -4.5, 0.0, 1.0]
+TIE_CODES_EVEN = [127, 0, 2, 2, 4, 0, -2, -2, -4, 126, -126, 4, -4, 0, 1]
+
+
+@pytest.mark.parametrize("moment", ["i8", "i8r64"])
+def test_int8_exact_ties_round_half_even(moment):
+    n = len(TIE_VALUES)
+    ties = np.array(TIE_VALUES)
+    if moment == "i8":                        # a 256-row block of each column: G[p, q] = dY[0, p]
+        d_in, d_out = 64, 256
+        X, dY = np.ones((1, d_in)), np.zeros((1, d_out))
+        dY[0, :n] = ties
+        zeros = np.zeros((d_out, d_in))
+        m, ms = oracle.quantize_i8(zeros, False)
+        v, vs = oracle.quantize_i8(zeros, True)
+    else:                                     # a 64-wide block of each row: G[p, q] = X[0, q]
+        d_in, d_out = 64, 8
+        X, dY = np.zeros((1, d_in)), np.ones((1, d_out))
+        X[0, :n] = ties
+        zeros = np.zeros((d_out, d_in))
+        m, ms = oracle.quantize_i8_row64(zeros, False)
+        v, vs = oracle.quantize_i8_row64(zeros, True)
+    b16 = lambda a: oracle.f64_to_bf16_bits(a)
+    assert np.array_equal(oracle.bf16_bits_to_f64(b16(ties)), ties)
+    hp = dict(lr=1e-3, beta1=0.0, beta2=0.0, eps=1e-8, weight_decay=0.1)
+    p = Problem(b16(X), b16(dY), b16(zeros), m, v, moment, ms, vs, hp=hp)
+    ora = run_oracle(p, 1)
+    gpu = run_gpu(p, 1)
+    _say(check_step(gpu, ora, moment, hp=hp))
+    assert np.array_equal(gpu["m"], ora["m"]), "m codes differ from the oracle at exact ties"
+    got = gpu["m"][:n, :] if moment == "i8" else gpu["m"][:, :n].T
+    assert (got == np.array(TIE_CODES_EVEN)[:, None]).all()
+    assert (gpu["m_scale"] == 1.0).all()

@@ -65,8 +65,12 @@ def run_rule(name, T, d_in, d_out, kind, step, seed=300):
     opt = RULES[name]
     h = lambda t: bits(t) if t is not None else None
     G = oracle.wgrad(bits(X), bits(dY))
-    ora = oracle.rule_step(G, bits(W), h(s1), h(s2), opt=opt,
-                           state_dtype=oracle.MOMENT_F32 if kind == "f32" else oracle.MOMENT_BF16, step=step, **hp)
+    EG = gemm_error_bound(bits(X), bits(dY))
+    sdt = oracle.MOMENT_F32 if kind == "f32" else oracle.MOMENT_BF16
+    ora = oracle.rule_step(G, bits(W), h(s1), h(s2), opt=opt, state_dtype=sdt, step=step, **hp)
+    # the oracle's W' at the ends of the interval the kernel's fp32 G lies in
+    W_at = lambda sign: oracle.rule_step(G + sign * EG, bits(W), h(s1), h(s2), opt=opt, state_dtype=sdt,
+                                         step=step, **hp)["W64"]
     g = [dev(bits(t)) if t is not None else None for t in (X, dY, W, s1, s2)]
     forge.forge_linear_step_opt(g[0], g[1], None if name == "muon_accumulate" else g[2], g[3], g[4],
                                 optimizer=name, step=step, **hp)
@@ -75,8 +79,7 @@ def run_rule(name, T, d_in, d_out, kind, step, seed=300):
     W64 = oracle.bf16_bits_to_f64(bits(W))
     to64 = lambda t: (oracle.bf16_bits_to_f64(bits(t)) if t.dtype == torch.bfloat16 else bits(t).astype(np.float64)) \
         if t is not None else None
-    return check_rule_step(gpu, ora, opt, kind, hp, G, gemm_error_bound(bits(X), bits(dY)), W64,
-                           to64(s1), to64(s2))
+    return check_rule_step(gpu, ora, opt, kind, hp, G, EG, W64, to64(s1), to64(s2), W_at=W_at)
 
 
 SHAPES = [(77, 328, 200), (256, 264, 520)]

@@ -814,3 +814,104 @@ def test_fp8_weight_update_reads_decoded_state():
     np.testing.assert_allclose(o["W64"], W1, rtol=1e-14)
     np.testing.assert_allclose(o["m64"], m1, rtol=1e-14)
     np.testing.assert_allclose(o["v64"], v1, rtol=1e-14)
+
+
+# ------------------------------------------------------------------------- int8 rounding ties
+
+# App. B rounds x/s to an integer code; the oracle reads "round" as round half to even
+# (ties to the even integer).  With a block absmax of exactly 127 the fp32 scale is exactly
+# 1 and every quotient is its value, so exact half-integers are ties.  Round half away from
+# zero (roundf), round half up (floor(x + 1/2)) and truncation each give different codes on
+# at least one of these.
+TIE_VALUES = [127.0, 0.5, 1.5, 2.5, 3.5, -0.5, -1.5, -2.5, -3.5, 126.5, -126.5, 4.5, -4.5, 0.0, 1.0]
+TIE_CODES_EVEN = [127, 0, 2, 2, 4, 0, -2, -2, -4, 126, -126, 4, -4, 0, 1]
+
+
+def test_round_half_even_codes_differ_from_other_tie_rules():
+    """The expected codes above are not those of the other plausible rounding rules."""
+    x = np.array(TIE_VALUES)
+    away = np.sign(x) * np.floor(np.abs(x) + 0.5)
+    up = np.floor(x + 0.5)
+    assert not np.array_equal(away, TIE_CODES_EVEN)
+    assert not np.array_equal(up, TIE_CODES_EVEN)
+    assert not np.array_equal(np.trunc(x), TIE_CODES_EVEN)
+
+
+def test_i8_column_quantizer_rounds_ties_to_even():
+    """256-row column blocks: one column holds the tie values (rest zero), absmax 127."""
+    d_out, d_in = 256, 3
+    x = np.zeros((d_out, d_in))
+    x[:len(TIE_VALUES), 1] = TIE_VALUES
+    x[::-1][:len(TIE_VALUES), 2] = TIE_VALUES       # the same values at the block's far end
+    codes, scales = oracle.quantize_i8(x, second_moment=False)
+    assert scales[0, 1] == 1.0 and scales[0, 2] == 1.0 and scales[0, 0] == 0.0
+    assert codes[:len(TIE_VALUES), 1].tolist() == TIE_CODES_EVEN
+    assert codes[::-1][:len(TIE_VALUES), 2].tolist() == TIE_CODES_EVEN
+    assert not codes[len(TIE_VALUES):, 1].any()
+
+
+def test_i8_column_quantizer_second_moment_ties_through_the_square_root():
+    """sqrt(v) is stored: v = r^2 for the non-negative tie values r (exact squares, exact
+    roots), so the codes are round-half-even(r), floored at 1 in a non-zero block."""
+    r = np.array([127.0, 0.5, 1.5, 2.5, 3.5, 126.5, 4.5, 0.0, 1.0])
+    v = np.zeros((256, 1))
+    v[:len(r), 0] = r * r
+    codes, scales = oracle.quantize_i8(v, second_moment=True)
+    assert scales[0, 0] == 1.0
+    # 0.5 -> 0 -> floored to 1; 0 -> 0 -> floored to 1
+    assert codes[:len(r), 0].tolist() == [127, 1, 2, 2, 4, 126, 4, 1, 1]
+
+
+def test_i8_row64_quantizer_rounds_ties_to_even():
+    """64-wide row blocks: the tie values in one block of a row, absmax 127; a second row
+    holds them at the end of a ragged last block."""
+    d_out, d_in = 2, 64 + 20
+    x = np.zeros((d_out, d_in))
+    x[0, 3:3 + len(TIE_VALUES)] = TIE_VALUES
+    x[1, 64 + 20 - len(TIE_VALUES):] = TIE_VALUES
+    codes, scales = oracle.quantize_i8_row64(x, second_moment=False)
+    assert scales[0, 0] == 1.0 and scales[1, 1] == 1.0
+    assert codes[0, 3:3 + len(TIE_VALUES)].tolist() == TIE_CODES_EVEN
+    assert codes[1, 64 + 20 - len(TIE_VALUES):].tolist() == TIE_CODES_EVEN
+
+
+def _tie_step(moment_dtype, layout_shape):
+    """One AdamW step with beta1 = beta2 = 0, so m' = G and v' = G^2 exactly; G holds the
+    tie values in one int8 block, which therefore has absmax 127 and scale 1."""
+    d_out, d_in = layout_shape
+    G = np.zeros((d_out, d_in))
+    W = np.zeros((d_out, d_in), dtype=np.uint16)
+    if moment_dtype == MOMENT_I8:
+        G[:len(TIE_VALUES), 0] = TIE_VALUES
+        mq, ms = oracle.quantize_i8(np.zeros((d_out, d_in)), False)
+        vq, vs = oracle.quantize_i8(np.zeros((d_out, d_in)), True)
+    else:
+        G[0, :len(TIE_VALUES)] = TIE_VALUES
+        mq, ms = oracle.quantize_i8_row64(np.zeros((d_out, d_in)), False)
+        vq, vs = oracle.quantize_i8_row64(np.zeros((d_out, d_in)), True)
+    out = oracle.adamw(G, W, mq, vq, m_scale=ms, v_scale=vs, moment_dtype=moment_dtype, step=1,
+                       want_quotients=True, **dict(HP, beta1=0.0, beta2=0.0))
+    return G, out
+
+
+def test_i8_column_step_rounds_ties_to_even():
+    G, out = _tie_step(MOMENT_I8, (256, 2))
+    n = len(TIE_VALUES)
+    np.testing.assert_array_equal(out["m64"][:n, 0], TIE_VALUES)
+    assert out["m_scale"][0, 0] == 1.0 and out["v_scale"][0, 0] == 1.0
+    assert out["m"][:n, 0].tolist() == TIE_CODES_EVEN
+    # sqrt(v') = |G|: codes round-half-even(|G|), floored at 1
+    want_v = [max(1, abs(c)) for c in TIE_CODES_EVEN]
+    assert out["v"][:n, 0].tolist() == want_v
+    np.testing.assert_array_equal(out["qm"][:n, 0], TIE_VALUES)
+
+
+def test_i8_row64_step_rounds_ties_to_even():
+    G, out = _tie_step(MOMENT_I8_ROW64, (1, 64))
+    n = len(TIE_VALUES)
+    assert out["m_scale"][0, 0] == 1.0
+    assert out["m"][0, :n].tolist() == TIE_CODES_EVEN
+    # v itself is stored (no square root): v' = G^2 with absmax 127^2, scale 127^2/127 = 127;
+    # quotients G^2/127 are not ties, so only check the floor and the absmax code here
+    assert out["v_scale"][0, 0] == np.float32(127.0 * 127.0) / np.float32(127.0)
+    assert out["v"][0, 0] == 127 and out["v"][0, n - 2] >= 1 and out["v"][0, n - 2] == 1
