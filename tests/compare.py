@@ -6,7 +6,8 @@ The bar (fused step, every config):
   ulp (2^-8 relative) is wider than 1e-3, so a neighbouring bf16 value is also accepted
   when the oracle's unrounded fp64 value lies within the kernel's own error bound of the
   midpoint between the two: there the kernel's fp32 value may legitimately round the
-  other way.  The bound is derived from the arithmetic: the fp32 accumulation of G in any
+  other way.  The bf16 rounding of the exact value's fp32 rounding is accepted as well
+  (double rounding through fp32, which any fp32 kernel that stores bf16 does).  The bound is derived from the arithmetic: the fp32 accumulation of G in any
   order errs by at most E_G = T 2^-24 (|dY|^T |X|) (the only discrepancy App. A's
   floating-point remark admits), which the moment recurrences scale by (1-beta1) and
   (1-beta2) 2|G|, plus a few fp32 roundings of the epilogue.  Every such allowance is
@@ -51,6 +52,12 @@ def bf16_key(bits: np.ndarray) -> np.ndarray:
     """Monotone integer key of bf16 bit patterns (adjacent values differ by 1; +0 == -0)."""
     b = bits.astype(np.int32)
     return np.where(b & 0x8000, -(b & 0x7FFF), b)
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """fp32 values -> bf16 bit patterns, round to nearest even (finite inputs)."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
 
 
 def bf16_f64(bits: np.ndarray) -> np.ndarray:
@@ -132,7 +139,13 @@ def check_moment(gpu: np.ndarray, ora: np.ndarray, ora64: np.ndarray, kind: str,
     tol = 1e-3 * np.abs(o) + 1e-6 * np.abs(o).max(initial=0.0)
     bad = np.abs(g - o) > tol
     allowed = np.zeros_like(bad)
+    double_rounded = np.zeros_like(bad)
     if kind == "bf16" and bad.any():
+        # the kernel stores bf16 of an fp32 value: bf16(fp32(exact)) is what exact fp32
+        # arithmetic gives, and it differs from bf16(exact) where the fp32 rounding lands on a
+        # bf16 midpoint (structurally common, e.g. 0.9 * m with a bf16 m at G = 0)
+        double_rounded = bad & (gpu == f32_to_bf16_bits(ora64.astype(np.float32)))
+        bad = bad & ~double_rounded
         kg, ko = bf16_key(gpu), bf16_key(ora)
         adjacent = np.abs(kg - ko) == 1
         mid = 0.5 * (g + o)
@@ -144,7 +157,8 @@ def check_moment(gpu: np.ndarray, ora: np.ndarray, ora64: np.ndarray, kind: str,
         # fp32 state is stored as computed: it must lie within the derived window of the exact
         # value (a much tighter bar than 1e-3 relative)
         fail |= np.abs(g - ora64) > window + U32 * np.abs(ora64)
-    stats = dict(n=int(gpu.size), allowance_hits=int(allowed.sum()), failures=int(fail.sum()))
+    stats = dict(n=int(gpu.size), allowance_hits=int(allowed.sum()), double_rounded=int(double_rounded.sum()),
+                 failures=int(fail.sum()))
     if fail.any():
         idx = np.argwhere(fail)[:5]
         ex = [(tuple(i), float(g[tuple(i)]), float(o[tuple(i)]), float(ora64[tuple(i)])) for i in idx]
