@@ -97,7 +97,9 @@ typedef enum {
     FORGE_ERR_ALIASING = 7,          /* an output overlaps another tensor */
     FORGE_ERR_NO_DEVICE = 8,         /* no usable gfx950 device is current */
     FORGE_ERR_LAUNCH = 9,            /* the kernel launch failed (hipGetLastError) */
-    FORGE_ERR_INVALID_OPTIMIZER = 10 /* unknown optimizer code */
+    FORGE_ERR_INVALID_OPTIMIZER = 10,/* unknown optimizer code */
+    FORGE_ERR_SCRATCH_LIMIT = 11     /* the problem needs more than the library's fixed
+                                        FORGE_SCRATCH_BYTES buffer (forge_linear_step_unfused_noalloc) */
 } forge_status;
 
 /*
@@ -348,6 +350,39 @@ FORGE_API forge_status forge_linear_step_unfused(const void *X, const void *dY, 
                                        float lr, float beta1, float beta2, float eps,
                                        float weight_decay, int64_t step, void *G_ws,
                                        int32_t grad_dtype, void *stream);
+
+/* Size in bytes of the library's fixed device buffer (one per device, held from the
+   library's load until the process ends). */
+#define FORGE_SCRATCH_BYTES (64LL << 20)
+
+/*
+ * forge_linear_step_unfused_noalloc -- forge_linear_step_unfused for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid allocation.  The gradient G goes to the library's fixed device buffer of
+ * FORGE_SCRATCH_BYTES instead of a caller workspace; the call allocates nothing (no
+ * hipMalloc, no allocating library routine) and otherwise behaves as
+ * forge_linear_step_unfused with `grad_dtype` for G: the results are bit-identical.
+ *
+ *   arguments   as in forge_linear_step_unfused, without G_ws
+ *
+ * Errors: as forge_linear_step_unfused; d_in * d_out * (2 for bf16, 4 for fp32) above
+ * FORGE_SCRATCH_BYTES: FORGE_ERR_SCRATCH_LIMIT (checked on the host after the shapes,
+ * before any HIP call); FORGE_ERR_LAUNCH if the buffer's device address cannot be obtained.
+ * The buffer is shared by every call on a device and keeps the last call's G: calls that
+ * overlap on one device (two streams, two host threads) race and must be serialised by the
+ * caller.  Nothing needs clearing between calls: the GEMM writes every element of G that
+ * the optimizer kernel then reads.  Set-up: the first call on a device looks up the
+ * buffer's device address (hipGetSymbolAddress, with that device current); the HIP
+ * runtime may load the library's code object that holds the buffer at that moment (its
+ * FORGE_SCRATCH_BYTES, held until the process ends), so a caller under graph capture or a
+ * no-allocation harness makes one call outside it first.
+ */
+FORGE_API forge_status forge_linear_step_unfused_noalloc(const void *X, const void *dY, void *W, void *m,
+                                                         void *v, float *m_scale, float *v_scale, int64_t T,
+                                                         int64_t d_in, int64_t d_out, int32_t moment_dtype,
+                                                         float lr, float beta1, float beta2, float eps,
+                                                         float weight_decay, int64_t step, int32_t grad_dtype,
+                                                         void *stream);
 
 /* Static description of a status code (never NULL). */
 FORGE_API const char *forge_status_string(int32_t status);

@@ -10,7 +10,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libforge.so")
-SOURCES = [os.path.join(CSRC, f) for f in ("forge_kernels.hip", "forge_dx.hip", "forge_api.cpp")]
+SOURCES = [os.path.join(CSRC, f) for f in ("forge_kernels.hip", "forge_dx.hip", "forge_scratch.hip",
+                                           "forge_api.cpp")]
 HEADERS = [os.path.join(CSRC, "forge_internal.h"), os.path.join(CSRC, "forge_device.h"),
            os.path.join(INCLUDE, "forge.h")]
 

@@ -377,6 +377,8 @@ const char *forge_status_string(int32_t s)
     case FORGE_ERR_NO_DEVICE: return "FORGE_ERR_NO_DEVICE: no gfx950 device is current";
     case FORGE_ERR_LAUNCH: return "FORGE_ERR_LAUNCH: kernel launch failed";
     case FORGE_ERR_INVALID_OPTIMIZER: return "FORGE_ERR_INVALID_OPTIMIZER: unknown optimizer code";
+    case FORGE_ERR_SCRATCH_LIMIT:
+        return "FORGE_ERR_SCRATCH_LIMIT: the gradient does not fit the library's fixed FORGE_SCRATCH_BYTES buffer";
     default: return "unknown forge_status";
     }
 }
@@ -683,6 +685,42 @@ forge_status forge_linear_step_unfused(const void *X, const void *dY, void *W, v
     if ((s = forge_wgrad(X, dY, G_ws, T, d_in, d_out, gd, stream)) != FORGE_OK) return s;
     return forge_adamw(G_ws, gd, W, m, v, m_scale, v_scale, d_in, d_out, md, lr, beta1, beta2,
                        eps, weight_decay, step, stream);
+}
+
+static_assert(FORGE_SCRATCH_BYTES == forge_impl::SCRATCH_BYTES, "scratch size of the ABI and the library");
+
+forge_status forge_linear_step_unfused_noalloc(const void *X, const void *dY, void *W, void *m, void *v,
+                                               float *m_scale, float *v_scale, int64_t T, int64_t d_in,
+                                               int64_t d_out, int32_t md, float lr, float beta1, float beta2,
+                                               float eps, float weight_decay, int64_t step, int32_t gd,
+                                               void *stream)
+{
+    forge_status s;
+    bool empty = false;
+    if ((s = check_dtype_moment(md)) != FORGE_OK) return s;
+    if (md == FORGE_MOMENT_FP8) return FORGE_ERR_INVALID_DTYPE;
+    if ((s = check_dtype_grad(gd)) != FORGE_OK) return s;
+    if ((s = check_shape(T, d_in, d_out, empty)) != FORGE_OK) return s;
+    if (empty) return FORGE_OK;
+    const int64_t g_bytes = (gd == FORGE_GRAD_F32 ? 4 : 2) * d_in * d_out;
+    if (g_bytes > FORGE_SCRATCH_BYTES) return FORGE_ERR_SCRATCH_LIMIT;
+    StateSet st;
+    if ((s = check_inputs(X, dY, T, d_in, d_out)) != FORGE_OK) return s;
+    if ((s = check_state(W, m, v, m_scale, v_scale, d_in, d_out, md, st)) != FORGE_OK) return s;
+    if ((s = check_hyper(lr, beta1, beta2, eps, weight_decay, step)) != FORGE_OK) return s;
+    if (T > 0 && (!disjoint_from(st, range_of(X, 2 * T * d_in)) || !disjoint_from(st, range_of(dY, 2 * T * d_out))))
+        return FORGE_ERR_ALIASING;
+    if ((s = check_device()) != FORGE_OK) return s;
+    void *G = nullptr;
+    if (forge_impl::scratch_address(&G) != hipSuccess) {
+        (void)hipGetLastError();
+        return FORGE_ERR_LAUNCH;
+    }
+    // The library's buffer is disjoint from every caller tensor; the two calls below
+    // validate again (cheaply) and launch the GEMM, then the optimizer, on `stream`.
+    if ((s = forge_wgrad(X, dY, G, T, d_in, d_out, gd, stream)) != FORGE_OK) return s;
+    return forge_adamw(G, gd, W, m, v, m_scale, v_scale, d_in, d_out, md, lr, beta1, beta2, eps, weight_decay,
+                       step, stream);
 }
 
 }  // extern "C"

@@ -109,4 +109,11 @@ hipError_t launch_dx(const DxSeg *s, int n, uint16_t *dX, int T, int d_in, hipSt
 // Compute units of the current device (cached per device ordinal; 256 if unknown).
 int device_cu_count();
 
+// The fixed device buffer of forge_linear_step_unfused_noalloc (forge_scratch.hip): its
+// size, and its address on the current device (looked up once per device ordinal below
+// MAX_DEVICES).
+constexpr int64_t SCRATCH_BYTES = int64_t(64) << 20;
+constexpr int MAX_DEVICES = 64;
+hipError_t scratch_address(void **out);
+
 }  // namespace forge_impl

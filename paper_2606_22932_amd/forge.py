@@ -23,7 +23,10 @@ STATUS = {
     3: "FORGE_ERR_UNSUPPORTED_SHAPE", 4: "FORGE_ERR_INVALID_HYPERPARAM",
     5: "FORGE_ERR_INVALID_DTYPE", 6: "FORGE_ERR_MISALIGNED", 7: "FORGE_ERR_ALIASING",
     8: "FORGE_ERR_NO_DEVICE", 9: "FORGE_ERR_LAUNCH", 10: "FORGE_ERR_INVALID_OPTIMIZER",
+    11: "FORGE_ERR_SCRATCH_LIMIT",
 }
+# bytes of the library's fixed device buffer (FORGE_SCRATCH_BYTES)
+FORGE_SCRATCH_BYTES = 64 << 20
 # forge_optimizer codes of include/forge.h
 OPTIMIZERS = {"adamw": 0, "sgd": 1, "sgd_momentum": 2, "adagrad": 3, "rmsprop": 4, "lion": 5, "nadam": 6,
               "radam": 7, "adamax": 8, "muon_accumulate": 9}
@@ -76,6 +79,8 @@ _SIGS = {
     "forge_adamw": [_P, _I32, _P, _P, _P, _P, _P, _I64, _I64, _I32, _F, _F, _F, _F, _F, _I64, _P],
     "forge_linear_step_unfused": [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I32, _F, _F, _F, _F,
                                   _F, _I64, _P, _I32, _P],
+    "forge_linear_step_unfused_noalloc": [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I32, _F, _F, _F, _F,
+                                          _F, _I64, _I32, _P],
     "forge_status_string": [_I32],
     "forge_query_tile": [_I32, ctypes.POINTER(_I32), ctypes.POINTER(_I32), ctypes.POINTER(_I32)],
 }
@@ -371,3 +376,17 @@ def forge_linear_step_unfused(X, dY, W, m, v, m_scale=None, v_scale=None, *, G_w
                                          _moment_code(m, m_scale), lr, beta1, beta2, eps, weight_decay,
                                          int(step), _ptr(G_ws), _grad_code(G_ws), _stream(stream, W))
     _check(st, "forge_linear_step_unfused")
+
+
+def forge_linear_step_unfused_noalloc(X, dY, W, m, v, m_scale=None, v_scale=None, *, grad_dtype, lr, beta1,
+                                      beta2, eps, weight_decay, step, stream=None):
+    """forge_linear_step_unfused with G in the library's fixed device buffer: allocates
+    nothing.  grad_dtype: "bf16" or "f32"."""
+    _dev(X, dY, W, m, v, m_scale, v_scale)
+    T, d_in, d_out = _shapes(X, dY, W)
+    gd = {"bf16": FORGE_GRAD_BF16, "f32": FORGE_GRAD_F32}[grad_dtype]
+    st = lib().forge_linear_step_unfused_noalloc(_ptr(X), _ptr(dY), _ptr(W), _ptr(m), _ptr(v),
+                                                 _ptr(m_scale), _ptr(v_scale), T, d_in, d_out,
+                                                 _moment_code(m, m_scale), lr, beta1, beta2, eps, weight_decay,
+                                                 int(step), gd, _stream(stream, W))
+    _check(st, "forge_linear_step_unfused_noalloc")

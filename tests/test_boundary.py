@@ -54,7 +54,7 @@ def test_library_exports_every_header_function():
 
 
 def test_status_strings():
-    for code in range(10):
+    for code in range(12):
         s = forge.forge_status_string(code)
         assert s.startswith(forge.STATUS[code])
     assert "unknown" in forge.forge_status_string(99)
@@ -448,3 +448,35 @@ def test_fp8_valid_arguments_reach_the_device_check():
     assert call_wfp8() == NODEV
     assert call_wfp8(md=FP8) == NODEV
     assert call_wfp8(m=BASE["W"] + 128 * 256) == NODEV           # right after a 1-byte-per-element W
+
+
+def call_noalloc(T=64, d_in=128, d_out=256, md=BF16, gd=0, **over):
+    a = dict(BASE)
+    a.update({k: v for k, v in over.items() if k in a})
+    hp = dict(HP)
+    hp.update({k: v for k, v in over.items() if k in hp})
+    return lib().forge_linear_step_unfused_noalloc(a["X"], a["dY"], a["W"], a["m"], a["v"], a["ms"], a["vs"], T,
+                                                   d_in, d_out, md, hp["lr"], hp["beta1"], hp["beta2"], hp["eps"],
+                                                   hp["wd"], hp["step"], gd, None)
+
+
+def test_noalloc_refuses_gradients_beyond_the_buffer():
+    """The fixed buffer holds FORGE_SCRATCH_BYTES: d_in * d_out * (2 or 4 bytes) beyond it is
+    FORGE_ERR_SCRATCH_LIMIT, refused on the host before any other pointer or device check."""
+    SCRATCH = 11
+    assert forge.FORGE_SCRATCH_BYTES == 64 << 20
+    assert call_noalloc(d_in=8192, d_out=4104, gd=0) == SCRATCH           # 67,239,936 B of bf16
+    assert call_noalloc(d_in=4096, d_out=4104, gd=1) == SCRATCH           # fp32
+    assert call_noalloc(d_in=4096, d_out=4104, gd=1, W=0) == SCRATCH      # before the pointer checks
+    # exactly the buffer passes the size check (the invalid step is caught after it, so no
+    # call here gets as far as a launch)
+    assert call_noalloc(d_in=8192, d_out=4096, gd=0, step=0) == HYPER
+    assert call_noalloc(d_in=4096, d_out=4096, gd=1, step=0) == HYPER
+    # the other rules are those of forge_linear_step_unfused
+    assert call_noalloc(gd=2) == DTYPE
+    assert call_noalloc(md=4) == DTYPE
+    assert call_noalloc(W=0) == NULLP
+    assert call_noalloc(step=0) == HYPER
+    assert call_noalloc(W=BASE["W"] + 2) == MISAL
+    assert call_noalloc(W=BASE["X"]) == ALIAS
+    assert call_noalloc(d_out=0) == OK
