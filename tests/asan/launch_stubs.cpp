@@ -24,5 +24,6 @@ hipError_t launch_wgrad(const Args &, int, hipStream_t) { unreachable("launch_wg
 hipError_t launch_adamw(const Args &, int, int, hipStream_t) { unreachable("launch_adamw"); }
 hipError_t launch_dx(const DxSeg *, int, uint16_t *, int, int, hipStream_t) { unreachable("launch_dx"); }
 int device_cu_count() { unreachable("device_cu_count"); }
+hipError_t scratch_address(void **) { unreachable("scratch_address"); }
 
 }  // namespace forge_impl
