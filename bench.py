@@ -188,6 +188,143 @@ def cpu_baseline(wl, device, budget_s=10.0):
                        "fp64 oracle time only (input transfer excluded)")
 
 
+def _median(xs):
+    xs = sorted(xs)
+    n = len(xs)
+    return xs[n // 2] if n % 2 else 0.5 * (xs[n // 2 - 1] + xs[n // 2])
+
+
+def time_batches(units, fn, per_batch, batches, warmup):
+    """Median (and range) over `batches` batches of the per-launch time in ms: each batch is
+    `per_batch` launches back to back between two HIP events on the launch stream, cycling
+    through `units` (rotated copies of the state, or a step sequence)."""
+    import torch
+    stream = torch.cuda.current_stream()
+    for i in range(warmup):
+        fn(units[i % len(units)], i)
+    k = warmup
+    times = []
+    for _ in range(batches):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(per_batch):
+            fn(units[k % len(units)], k)
+            k += 1
+        b.record(stream)
+        b.synchronize()
+        times.append(a.elapsed_time(b) / per_batch)
+    return _median(times), min(times), max(times)
+
+
+def oracle_seconds(args, kwargs, runs, threads):
+    """Median wall time of `runs` oracle steps on `threads` host threads (oracle call only)."""
+    import oracle
+    oracle.set_num_threads(threads)
+    ts = []
+    for _ in range(runs):
+        t0 = time.perf_counter()
+        oracle.linear_step(*args, **kwargs)
+        ts.append(time.perf_counter() - t0)
+    return _median(ts)
+
+
+# The single-layer configurations reported beside the sweep: C1 (layer256, fp32 moments,
+# steps 1-3), C2 (o_proj), C3 (the MLP projections, bf16 moments), C4 (the same, int8 moments
+# in 256-row column blocks).  C2's 210 MB fits the 256 MB Infinity Cache, so it is timed over
+# ROTATE_C2 copies of its inputs and state, launched in turn.
+ROTATE_C2 = 3
+CONFIG_NAMES = {"C1": "layer256", "C2": "o_proj", "C3": "mlp", "C4": "mlp_i8"}
+
+
+def single_configs(device, cores):
+    """Per-config GPU time, GB/s and % of 8 TB/s, each next to the fp64 oracle on the host's
+    cores (and, for C1 and C2, on one thread).  GPU: median over batches of back-to-back
+    launches; oracle: median of 3 runs (C1, C2) or one run per matrix (C3, C4)."""
+    import numpy as np
+    import oracle
+    import torch
+    from paper_2606_22932_amd import accounting, forge, synth
+    b16 = lambda t: t.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+    host = lambda t: b16(t) if t.dtype == torch.bfloat16 else t.detach().cpu().contiguous().numpy()
+    out = {}
+    for key, name in CONFIG_NAMES.items():
+        wl = synth.WORKLOADS[name]
+        hp = wl.hyper
+        log(f"config {key} ({name}): GPU")
+        copies = ROTATE_C2 if key == "C2" else 1
+        per_mat = []                     # per matrix: list of copies of its launch arguments
+        for mat in wl.matrices:
+            cs = []
+            for c in range(copies):
+                X, dY = synth.activations(wl.T, mat, wl, wl.steps[0], device=device)
+                W = synth.weight(mat, wl, device=device)
+                if wl.moment == "i8":
+                    m, v, ms, vs = synth.random_i8_state(mat, wl, device=device, layout="col256")
+                else:
+                    dt = torch.float32 if wl.moment == "f32" else torch.bfloat16
+                    m, v = synth.warm_moments(mat, wl, device=device, dtype=dt)
+                    ms = vs = None
+                dYs = [synth.activations(wl.T, mat, wl, t, device=device)[1] for t in wl.steps] \
+                    if len(wl.steps) > 1 else [dY]
+                cs.append(dict(X=X, dYs=dYs, W=W, m=m, v=v, ms=ms, vs=vs))
+            per_mat.append(cs)
+        torch.cuda.synchronize()
+        nsteps = len(wl.steps)
+
+        def launch(c, k):
+            j = k % nsteps          # C1 cycles through its steps 1..3 with their own dY
+            forge.forge_linear_step(c["X"], c["dYs"][j], c["W"], c["m"], c["v"], c["ms"], c["vs"],
+                                    step=wl.steps[j], **hp)
+
+        per_launch = 60 if key == "C1" else (30 if key == "C2" else 10)
+        ms_total, lo_total, hi_total = 0.0, 0.0, 0.0
+        for cs in per_mat:
+            med, lo, hi = time_batches(cs, launch, per_launch, 21, 3 * per_launch)
+            ms_total += med
+            lo_total += lo
+            hi_total += hi
+        fused_b = sum(accounting.fused_bytes(wl.T, m_.d_in, m_.d_out, wl.moment) for m_ in wl.matrices)
+        gbs = fused_b / (ms_total * 1e-3) / 1e9
+        r = {"workload": name, "T": wl.T, "matrices": [f"{m_.name}[{m_.d_out}x{m_.d_in}]" for m_ in wl.matrices],
+             "moments": wl.moment, "algorithmic_bytes": fused_b,
+             "gpu_us": round(ms_total * 1e3, 2), "gpu_us_range": [round(lo_total * 1e3, 2), round(hi_total * 1e3, 2)],
+             "gpu_GBs": round(gbs, 1), "frac_of_8TBs": round(gbs / HBM_PEAK_GBS, 4),
+             "timing": f"sum over matrices of the median of 21 batches of {per_launch} back-to-back launches"
+                       + (f", rotating {copies} copies of inputs and state" if copies > 1 else "")}
+        # the oracle on the host: the same inputs (first copy), the step's state as the GPU has it
+        log(f"config {key}: oracle on {cores} threads" + (" and 1 thread" if key in ("C1", "C2") else ""))
+        t_all, t_one = 0.0, 0.0
+        for mat, cs in zip(wl.matrices, per_mat):
+            c = cs[0]
+            if wl.moment == "i8":
+                # the timing state's codes and scales, on the host
+                mq, vq, ms_, vs_ = synth.random_i8_state(mat, wl, device=device, layout="col256")
+                args = (b16(c["X"]), b16(c["dYs"][0]), b16(c["W"]), host(mq), host(vq))
+                kw = dict(moment_dtype=oracle.MOMENT_I8, m_scale=host(ms_), v_scale=host(vs_))
+            else:
+                m0, v0 = synth.warm_moments(mat, wl, device=device,
+                                            dtype=torch.float32 if wl.moment == "f32" else torch.bfloat16)
+                args = (b16(c["X"]), b16(c["dYs"][0]), b16(c["W"]), host(m0), host(v0))
+                kw = dict(moment_dtype=oracle.MOMENT_F32 if wl.moment == "f32" else oracle.MOMENT_BF16)
+            kw.update(step=wl.steps[0], **hp)
+            runs = 3 if key in ("C1", "C2") else 1
+            t_all += oracle_seconds(args, kw, runs, cores)
+            if key in ("C1", "C2"):
+                t_one += oracle_seconds(args, kw, runs, 1)
+        oracle.set_num_threads(cores)
+        r["oracle"] = {"seconds": round(t_all, 4), "GBs": round(fused_b / t_all / 1e9, 4), "cores": cores,
+                       "runs": "median of 3" if key in ("C1", "C2") else "one run per matrix, summed"}
+        if key in ("C1", "C2"):
+            r["oracle_1_thread"] = {"seconds": round(t_one, 4), "GBs": round(fused_b / t_one / 1e9, 4), "cores": 1,
+                                    "runs": "median of 3"}
+        r["gpu_over_oracle"] = round(t_all / (ms_total * 1e-3), 1)
+        out[key] = r
+        log(f"config {key}: {r}")
+        del per_mat
+        torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -196,6 +333,8 @@ def main():
     ap.add_argument("--workload", default="sweep", choices=["sweep", "o_proj", "mlp", "mlp_i8", "mlp_i8r64"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the single-layer configurations C1-C4 (timed beside the sweep by default)")
     ap.add_argument("--tokens", type=int, default=None,
                     help="override the workload's token count T (0: the state streaming alone)")
     ap.add_argument("--no-ceilings", action="store_true",
@@ -325,7 +464,9 @@ def main():
         ub = sum(accounting.unfused_bytes(T, d["mat"].d_in, d["mat"].d_out, wl.moment, "bf16") for d in mats)
         out["unfused"] = {"ms_per_step": round(ums, 4), "algorithmic_bytes_per_step": ub,
                           "GBs_of_fused_bytes": round(fused_b / (ums * 1e-3) / 1e9, 2),
-                          "speedup_fused_over_unfused": round(ums / ms, 4)}
+                          "GBs_of_unfused_bytes": round(ub / (ums * 1e-3) / 1e9, 2),
+                          "speedup_fused_over_unfused": round(ums / ms, 4),
+                          "byte_ratio_unfused_over_fused": round(ub / fused_b, 4)}
         log(f"unfused: {ums:.3f} ms/step -> fused speedup {ums / ms:.3f}x")
         del G_ws
 
@@ -335,6 +476,12 @@ def main():
         log("timing the CPU oracle on its sample")
         out["cpu_baseline"] = cpu_baseline(synth.WORKLOADS["sweep"], device)
         log(f"cpu baseline: {out['cpu_baseline']}")
+
+    if not args.no_configs and args.workload == "sweep" and args.tokens is None:
+        mats = launches = None
+        torch.cuda.empty_cache()
+        import oracle
+        out["configs"] = single_configs(device, oracle.num_threads())
 
     if not args.no_ceilings:
         mats = launches = None

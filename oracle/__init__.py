@@ -86,6 +86,8 @@ def _load():
             lib.forge_oracle_rule_step.restype = None
             lib.forge_oracle_num_threads.argtypes = []
             lib.forge_oracle_num_threads.restype = I32
+            lib.forge_oracle_set_num_threads.argtypes = [I32]
+            lib.forge_oracle_set_num_threads.restype = None
             _lib = lib
     return _lib
 
@@ -104,6 +106,11 @@ def _c(a, dtype):
 def num_threads() -> int:
     """OpenMP threads the oracle runs with (OMP_NUM_THREADS, else all host cores)."""
     return int(_load().forge_oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads for the oracle's parallel loops from now on (n >= 1; used by timing runs)."""
+    _load().forge_oracle_set_num_threads(int(n))
 
 
 # ----------------------------------------------------------------------------- rounding

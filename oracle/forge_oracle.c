@@ -676,3 +676,14 @@ int forge_oracle_num_threads(void)
     return 1;
 #endif
 }
+
+/* Threads the oracle's parallel loops use from now on (n >= 1); for timing runs. */
+void forge_oracle_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    extern void omp_set_num_threads(int);
+    if (n >= 1) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
