@@ -89,7 +89,7 @@ def build_workload(wl, device, moment_override=None):
     return mats
 
 
-def time_steps(launches, wl, fn, steps, warmup, step0):
+def time_steps(launches, wl, fn, steps, warmup, step0, side_streams=()):
     """Run `warmup` untimed steps, then `steps` timed steps back to back on the current
     stream (the one the library launches on), bracketed by two HIP events on that stream.
 
@@ -108,9 +108,15 @@ def time_steps(launches, wl, fn, steps, warmup, step0):
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     start.record(stream)
+    for ss in side_streams:           # launches on other streams start after `start`
+        ss.wait_event(start)
     for s in range(steps):
         for unit in launches:
             fn(unit, step0 + warmup + s)
+    for ss in side_streams:           # ... and `end` waits for them
+        e = torch.cuda.Event()
+        e.record(ss)
+        stream.wait_event(e)
     end.record(stream)
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) * 1e3
@@ -333,6 +339,10 @@ def main():
     ap.add_argument("--workload", default="sweep", choices=["sweep", "o_proj", "mlp", "mlp_i8", "mlp_i8r64"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
+    ap.add_argument("--streams", type=int, default=1,
+                    help="launch consecutive sweep launches round-robin on this many streams")
+    ap.add_argument("--schedule", default="backward", choices=["backward", "layer"],
+                    help="sweep launch grouping: per backward-pass group, or one launch per layer")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the single-layer configurations C1-C4 (timed beside the sweep by default)")
     ap.add_argument("--tokens", type=int, default=None,
@@ -389,16 +399,24 @@ def main():
 
     # One fused launch per group of matrices whose gradients a backward pass makes available
     # together (one matrix per launch except q/k/v and gate/up of the sweep).
-    launches = [[mats[i] for i in g] for g in synth.launch_groups(wl)]
+    launches = [[mats[i] for i in g] for g in synth.launch_groups(wl, args.schedule)]
+
+    # Consecutive launches touch disjoint state, so they may run on alternating streams: the
+    # next launch's first tiles then start on the compute units that the previous launch's
+    # last tiles free, instead of after all of them have finished.
+    streams = [torch.cuda.current_stream()] + [torch.cuda.Stream() for _ in range(args.streams - 1)]
+    nlaunch = [0]
 
     def fused(group, t):
+        st = streams[nlaunch[0] % len(streams)]
+        nlaunch[0] += 1
         forge.forge_linear_step_grouped([(d["X"], d["dY"], d["W"], d["m"], d["v"], d["ms"], d["vs"])
-                                         for d in group], step=t, **hp)
+                                         for d in group], step=t, stream=st.cuda_stream, **hp)
 
     fused_b = sum(accounting.fused_bytes(T, d["mat"].d_in, d["mat"].d_out, wl.moment) for d in mats)
     flops = sum(accounting.gemm_flops(T, d["mat"].d_in, d["mat"].d_out) for d in mats)
     log(f"timing fused ({len(launches)} launches per step)")
-    total, wall = time_steps(launches, wl, fused, args.steps, args.warmup, wl.steps[0])
+    total, wall = time_steps(launches, wl, fused, args.steps, args.warmup, wl.steps[0], streams[1:])
     ms = total / args.steps
     avg_launch_ms = total / (args.steps * len(launches))
     kern_gbs = (fused_b / len(launches)) / (avg_launch_ms * 1e-3) / 1e9

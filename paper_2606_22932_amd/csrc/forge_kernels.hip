@@ -231,15 +231,15 @@ struct Mainloop {
 
     // Wait until this wave's DMA for the oldest in-flight chunk has landed (`younger`
     // chunks issued after it may stay in flight), then barrier so every wave's has.
+    template <int Y = NS - 2>
     static __device__ __forceinline__ void wait_chunk(int younger)
     {
         static_assert(DPC * (NS - 2) <= 63, "vmcnt range");
-        if (younger >= NS - 2) {
-            asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"i"(DPC * (NS - 2)) : "memory");
-        } else if (NS > 3 && younger == 1) {
-            asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"i"(DPC) : "memory");
-        } else {
+        if constexpr (Y == 0) {
             asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+        } else {
+            if (younger >= Y) asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"i"(DPC * Y) : "memory");
+            else wait_chunk<Y - 1>(younger);
         }
     }
 
@@ -487,7 +487,11 @@ struct EpiRule {
     // issued as the epilogue starts, AHEAD passes before their use.  With all eight passes
     // in flight at a workgroup's start the sweep ran 1.1 % slower (less state in flight
     // per CU suits in-place HBM traffic; fewer than six loses overlap with the GEMM).
+#ifdef FORGE_PF_AHEAD
+    static constexpr int AHEAD = FORGE_PF_AHEAD < M::NPASS ? FORGE_PF_AHEAD : M::NPASS;
+#else
     static constexpr int AHEAD = M::NPASS > 2 ? M::NPASS - 2 : M::NPASS;
+#endif
     u32x4_t pw[R::W_RW ? NPF : 1], ps1[R::NS >= 1 ? NPF : 1], ps2[R::NS >= 2 ? NPF : 1];
 
     // Loads of pass I (one row per lane) into the prefetch registers.
@@ -983,28 +987,36 @@ struct EpiAdamWI8 {
     u32x2_t pm[M::NPASS], pv[M::NPASS];
     float sm[8], sv[8];
 
+    // Loads are range-checked buffer loads: elements outside the matrix read as zero, and no
+    // branch splits the code per row.
+    __device__ __forceinline__ void load_w(const Args &a, int p0, int q0, int s, int i)
+    {
+        const int p = p0 + i * M::RPP + s / M::LPR, q = q0 + (s % M::LPR) * 8;
+        const uint64_t n = 2ull * (uint64_t)a.d_out * (uint64_t)a.d_in;
+        pw[i] = __builtin_amdgcn_raw_buffer_load_b128(rsrc_of(a.W, n), elem_off(p, q, a.d_out, a.d_in, 2), 0, 2);
+    }
+
     __device__ __forceinline__ void prefetch(const Args &a, int p0, int q0, int s)
     {
         const int rs = s / M::LPR, q = q0 + (s % M::LPR) * 8;
-        const bool qok = q < a.d_in;
+        const uint64_t n = (uint64_t)a.d_out * (uint64_t)a.d_in;
 #pragma unroll
         for (int i = 0; i < M::NPASS; ++i) {
             const int p = p0 + i * M::RPP + rs;
-            pw[i] = u32x4_t{0u, 0u, 0u, 0u};
-            pm[i] = pv[i] = u32x2_t{0u, 0u};
-            if (qok && p < a.d_out) {
-                const size_t off = (size_t)p * a.d_in + q;
-                pw[i] = ld_nt<u32x4_t>(a.W + off);
-                pm[i] = ld_nt<u32x2_t>(static_cast<const int8_t *>(a.m) + off);
-                pv[i] = ld_nt<u32x2_t>(static_cast<const int8_t *>(a.v) + off);
-            }
+            load_w(a, p0, q0, s, i);
+            const uint32_t off = elem_off(p, q, a.d_out, a.d_in, 1);
+            pm[i] = __builtin_amdgcn_raw_buffer_load_b64(rsrc_of(a.m, n), off, 0, 2);
+            pv[i] = __builtin_amdgcn_raw_buffer_load_b64(rsrc_of(a.v, n), off, 0, 2);
         }
-        f32x4_t s0 = {0, 0, 0, 0}, s1 = s0, t0 = s0, t1 = s0;
-        if (qok) {
-            const size_t so = (size_t)(p0 / I8_BLOCK) * a.d_in + q;
-            s0 = ld_nt<f32x4_t>(a.ms + so); s1 = ld_nt<f32x4_t>(a.ms + so + 4);
-            t0 = ld_nt<f32x4_t>(a.vs + so); t1 = ld_nt<f32x4_t>(a.vs + so + 4);
-        }
+        const int blk = p0 / I8_BLOCK, nblk = (a.d_out + I8_BLOCK - 1) / I8_BLOCK;
+        const uint64_t ns = 4ull * (uint64_t)nblk * (uint64_t)a.d_in;
+        const uint32_t so = elem_off(blk, q, nblk, a.d_in, 4);
+        const __amdgpu_buffer_rsrc_t rm = rsrc_of(a.ms, ns), rv = rsrc_of(a.vs, ns);
+        const uint32_t so4 = so == OOR_OFFSET ? so : so + 16u;
+        const f32x4_t s0 = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rm, so, 0, 2));
+        const f32x4_t s1 = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rm, so4, 0, 2));
+        const f32x4_t t0 = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rv, so, 0, 2));
+        const f32x4_t t1 = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rv, so4, 0, 2));
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             sm[e] = s0[e]; sm[e + 4] = s1[e];
@@ -1061,6 +1073,10 @@ struct EpiAdamWI8 {
                 for (int k = 0; k < 4; ++k) wn[k] = pack_bf16(wo[2 * k], wo[2 * k + 1]);
                 st_nt<u32x4_t>(a.W + (size_t)p * a.d_in + q, wn);
             }
+            // close this pass's absmax now: otherwise the compiler keeps every pass's m' and
+            // sqrt(v') live to combine them after the loop (200 VGPRs instead of ~100)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) asm volatile("" : "+v"(am[e]), "+v"(av[e]));
             __builtin_amdgcn_sched_barrier(0);
         }
         // lanes of one wave sharing these columns differ in the bits above log2(LPR)
@@ -1312,8 +1328,11 @@ struct StreamI8 {
         const int p = p0 + I * M::RPP + s / M::LPR, q = q0 + (s % M::LPR) * 8;
         const uint64_t n = (uint64_t)a.d_out * (uint64_t)a.d_in;
         const uint32_t off = elem_off(p, q, a.d_out, a.d_in, 1);
-        cm[I] = __builtin_amdgcn_raw_buffer_load_b64(rsrc_of(a.m, n), off, 0, 2);
-        cv[I] = __builtin_amdgcn_raw_buffer_load_b64(rsrc_of(a.v, n), off, 0, 2);
+        // Plain (not non-temporal) loads: a tile's 64-byte code rows are half of a 128-byte
+        // line whose other half the neighbouring tile reads a little later from L2 (mlp_i8:
+        // 314 instead of 334 MB fetched per launch).
+        cm[I] = __builtin_amdgcn_raw_buffer_load_b64(rsrc_of(a.m, n), off, 0, 0);
+        cv[I] = __builtin_amdgcn_raw_buffer_load_b64(rsrc_of(a.v, n), off, 0, 0);
     }
     __device__ __forceinline__ void load_scales(const Args &a, int p0, int q0, int s)
     {

@@ -82,7 +82,7 @@ def _sweep_matrices():
     return tuple(mats)
 
 
-def launch_groups(wl: "Workload"):
+def launch_groups(wl: "Workload", schedule: str = "backward"):
     """Indices into ``wl.matrices`` per fused launch, in the order a backward pass makes
     the weight gradients available.
 
@@ -96,6 +96,10 @@ def launch_groups(wl: "Workload"):
     per = len(LLAMA8B_PROJ)
     idx = {nm: j for j, (nm, _, _) in enumerate(LLAMA8B_PROJ)}
     groups = [[32 * per]]
+    if schedule == "layer":
+        # one launch per decoder layer, last layer first: the layer's input gradients are
+        # formed first (each from its pre-update weight), then its seven weights are stepped
+        return groups + [[layer * per + j for j in range(per)] for layer in reversed(range(32))]
     for layer in reversed(range(32)):
         b = layer * per
         groups += [[b + idx["down"]], [b + idx["gate"], b + idx["up"]], [b + idx["o"]],

@@ -480,3 +480,16 @@ def test_noalloc_refuses_gradients_beyond_the_buffer():
     assert call_noalloc(W=BASE["W"] + 2) == MISAL
     assert call_noalloc(W=BASE["X"]) == ALIAS
     assert call_noalloc(d_out=0) == OK
+
+
+def test_library_has_no_undefined_internal_symbols():
+    """Every kernel launch stub the library references is defined in it (a hipcc build that
+    drops a template kernel's host stub would fail to load only when that path is used)."""
+    import shutil
+    import subprocess
+    from paper_2606_22932_amd import build
+    nm = shutil.which("nm")
+    if nm is None:
+        pytest.skip("nm not available")
+    out = subprocess.run([nm, "-D", "--undefined-only", build.LIB], capture_output=True, text=True, check=True).stdout
+    assert "forge_impl" not in out, out
