@@ -1,6 +1,8 @@
 """The fused paths allocate no device memory: a call leaves torch's allocator and the
 device's free memory where they were (the library takes caller-owned buffers and keeps no
 workspace; the kernels need none)."""
+import gc
+
 import pytest
 import torch
 
@@ -35,6 +37,17 @@ def _snapshot():
     return torch.cuda.memory_allocated(), torch.cuda.memory_reserved(), torch.cuda.mem_get_info()[0]
 
 
+class _no_gc:
+    """Collect garbage first and keep the collector off inside the measured window, so that
+    tensors freed by an earlier test cannot lower the figures during the call."""
+    def __enter__(self):
+        gc.collect()
+        gc.disable()
+
+    def __exit__(self, *exc):
+        gc.enable()
+
+
 @pytest.mark.parametrize("moment", ["bf16", "i8", "i8r64"])
 def test_fused_step_grouped_and_backward_allocate_nothing(moment):
     X, mats = _mats(moment, 3)
@@ -47,9 +60,10 @@ def test_fused_step_grouped_and_backward_allocate_nothing(moment):
         forge.forge_linear_backward_grouped(mats, dX=dX, step=step, **HP)
 
     calls(1)                       # code objects loaded, first launches done
-    before = _snapshot()
-    for t in range(2, 5):
-        calls(t)
-    after = _snapshot()
+    with _no_gc():
+        before = _snapshot()
+        for t in range(2, 5):
+            calls(t)
+        after = _snapshot()
     print(f"{moment}: allocated/reserved/free before {before}, after {after}", flush=True)
     assert after == before

@@ -7,6 +7,8 @@ optimizer kernels on the same G), on two calls in a row with the second smaller 
 first, and at the buffer's maximum size.  The call must leave torch's allocator and the
 device's free memory unchanged, and a gradient larger than the buffer is refused.
 """
+import gc
+
 import pytest
 import torch
 
@@ -33,6 +35,17 @@ def _snapshot():
     return torch.cuda.memory_allocated(), torch.cuda.memory_reserved(), torch.cuda.mem_get_info()[0]
 
 
+class _no_gc:
+    """Collect garbage first and keep the collector off inside the measured window, so that
+    tensors freed by an earlier test cannot lower the figures during the call."""
+    def __enter__(self):
+        gc.collect()
+        gc.disable()
+
+    def __exit__(self, *exc):
+        gc.enable()
+
+
 @pytest.fixture(scope="module", autouse=True)
 def buffer_set_up():
     """The first call on a device looks up the buffer's address; the HIP runtime may load
@@ -50,9 +63,10 @@ def _compare(p, grad, step):
     a, b = _state(p), _state(p)
     G = torch.empty(p.W.shape, dtype=torch.bfloat16 if grad == "bf16" else torch.float32, device="cuda")
     forge.forge_linear_step_unfused(X, dY, *a, G_ws=G, step=step, **p.hp)
-    before = _snapshot()
-    forge.forge_linear_step_unfused_noalloc(X, dY, *b, grad_dtype=grad, step=step, **p.hp)
-    after = _snapshot()
+    with _no_gc():
+        before = _snapshot()
+        forge.forge_linear_step_unfused_noalloc(X, dY, *b, grad_dtype=grad, step=step, **p.hp)
+        after = _snapshot()
     assert after == before, f"allocation seen: {before} -> {after}"
     for x, y, name in zip(a, b, ("W", "m", "v", "m_scale", "v_scale")):
         if x is not None:
