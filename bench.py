@@ -34,30 +34,31 @@ COPY_BYTES = 1 << 30           # size of the calibration copy (--copy-calibratio
 # sources whose sha256 is recorded: after any change to them the figure is reported as null.
 TRAFFIC = {
     "sweep": {
-        "source_sha256": "2b76028b052c44212bbda669438c71bb741e59c0c7b53931571d553560e08d57",
-        "fetch_kib_per_launch": 206170.3,     # FETCH_SIZE, mean over the 129 launches of a step
-        "write_kib_per_launch": 340875.9,     # WRITE_SIZE
-        "fetch_scale": 1.99995,               # 1 GiB copy: FETCH_SIZE reads 524302 KiB
+        "source_sha256": "21b32061fcb0175866119c4f05eeaedec9b4e9ac242d30994ba693a73f1c3964",
+        "fetch_kib_per_launch": 206223.0,     # FETCH_SIZE, mean over the 129 launches of a step
+        "write_kib_per_launch": 340884.4,     # WRITE_SIZE
+        "fetch_scale": 1.99992,               # 1 GiB copy: FETCH_SIZE reads 524308 KiB
         "write_scale": 1.0,                   # 1 GiB copy: WRITE_SIZE reads 1048576 KiB
-        "bytes_per_launch": 771282175,        # (fetch * fetch_scale + write * write_scale) KiB
+        "bytes_per_launch": 771394305,        # (fetch * fetch_scale + write * write_scale) KiB
     },
     "mlp_i8": {
-        "source_sha256": "2b76028b052c44212bbda669438c71bb741e59c0c7b53931571d553560e08d57",
-        "fetch_kib_per_launch": 169535.5,     # mean over the 3 launches (gate, up, down)
-        "write_kib_per_launch": 252100.6,
-        "fetch_scale": 1.99995,
+        "source_sha256": "21b32061fcb0175866119c4f05eeaedec9b4e9ac242d30994ba693a73f1c3964",
+        "fetch_kib_per_launch": 153636.2,     # mean over the 3 launches (gate, up, down)
+        "write_kib_per_launch": 262406.3,
+        "fetch_scale": 1.99992,
         "write_scale": 1.0,
-        "bytes_per_launch": 605350295,
+        "bytes_per_launch": 583338663,
     },
     "mlp_i8r64": {
-        "source_sha256": "2b76028b052c44212bbda669438c71bb741e59c0c7b53931571d553560e08d57",
-        "fetch_kib_per_launch": 155877.2,     # mean over the 3 launches (gate, up, down)
-        "write_kib_per_launch": 239736.2,
-        "fetch_scale": 1.99995,
+        "source_sha256": "21b32061fcb0175866119c4f05eeaedec9b4e9ac242d30994ba693a73f1c3964",
+        "fetch_kib_per_launch": 155836.6,     # mean over the 3 launches (gate, up, down)
+        "write_kib_per_launch": 239203.4,
+        "fetch_scale": 1.99992,
         "write_scale": 1.0,
-        "bytes_per_launch": 564717741,
+        "bytes_per_launch": 564085583,
     },
 }
+
 
 # Default (warmup, timed) steps per workload when --steps / --warmup are not given: the
 # sweep's 20 ms steps need few; the single-matrix and MLP workloads get enough steps for
