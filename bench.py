@@ -63,8 +63,8 @@ TRAFFIC = {
 # Default (warmup, timed) steps per workload when --steps / --warmup are not given: the
 # sweep's 20 ms steps need few; the single-matrix and MLP workloads get enough steps for
 # about 0.1 s of warmup and 0.2 s of timed work, so that clocks and TLBs are warm.
-DEFAULT_STEPS = {"sweep": (3, 10), "o_proj": (2000, 4000), "mlp": (200, 400), "mlp_i8": (200, 300),
-                 "mlp_i8r64": (200, 400)}
+DEFAULT_STEPS = {"sweep": (3, 10), "o_proj": (2000, 4000), "o_proj_t4096": (300, 600), "mlp": (200, 400),
+                 "mlp_i8": (200, 300), "mlp_i8r64": (200, 400)}
 
 
 def log(*a):
@@ -193,6 +193,12 @@ def cpu_baseline(wl, device, budget_s=10.0):
                 sample=f"decoder layers 0-{layers - 1} of the sweep ({n_mats} matrices, "
                        f"{total_b / 1e9:.2f} GB algorithmic), T=512, bf16 moments, step 100; "
                        "fp64 oracle time only (input transfer excluded)")
+
+
+def compute_bound(T: int) -> bool:
+    """bf16 state: 2T GEMM flop against 12 B of state per parameter; the MFMA and HBM
+    roofs (2.5 PFLOP/s, 8 TB/s) cross at 2T/12 = 312.5 flop/B, i.e. T = 1875."""
+    return 2 * T / 12 > MFMA_BF16_PEAK_TFS * 1e12 / (HBM_PEAK_GBS * 1e9)
 
 
 def _median(xs):
@@ -332,12 +338,48 @@ def single_configs(device, cores):
     return out
 
 
+def compute_bound_block(device):
+    """The fused step past the ridge: Llama-3.1-8B o_proj (4096 x 4096) at T = 4096 (App. D's
+    BT = 4096), rotating 3 copies of inputs and state; next to it the store-G control (the
+    same tile kernel storing G in bf16 instead of updating the state) on the same inputs."""
+    import torch
+    from paper_2606_22932_amd import accounting, forge, synth
+    wl = synth.WORKLOADS["o_proj_t4096"]
+    mat = wl.matrices[0]
+    hp = wl.hyper
+    copies = []
+    for c in range(3):
+        X, dY = synth.activations(wl.T, mat, wl, wl.steps[0], device=device)
+        W = synth.weight(mat, wl, device=device)
+        m, v = synth.warm_moments(mat, wl, device=device, dtype=torch.bfloat16)
+        copies.append(dict(X=X, dY=dY, W=W, m=m, v=v))
+    G = torch.empty((mat.d_out, mat.d_in), dtype=torch.bfloat16, device=device)
+    fused = lambda c, k: forge.forge_linear_step(c["X"], c["dY"], c["W"], c["m"], c["v"], step=wl.steps[0], **hp)
+    store_g = lambda c, k: forge.forge_wgrad(c["X"], c["dY"], G)
+    f_ms, f_lo, f_hi = time_batches(copies, fused, 12, 11, 24)
+    g_ms, g_lo, g_hi = time_batches(copies, store_g, 12, 11, 24)
+    flops = accounting.gemm_flops(wl.T, mat.d_in, mat.d_out)
+    byts = accounting.fused_bytes(wl.T, mat.d_in, mat.d_out, wl.moment)
+    tf = lambda ms: flops / (ms * 1e-3) / 1e12
+    del copies, G
+    torch.cuda.empty_cache()
+    return {"workload": "Llama-3.1-8B o_proj 4096x4096, T=4096, bf16 W/m/v (rotating 3 copies)",
+            "gemm_flops": flops, "algorithmic_bytes": byts,
+            "fused_us": round(f_ms * 1e3, 2), "fused_us_range": [round(f_lo * 1e3, 2), round(f_hi * 1e3, 2)],
+            "fused_TFs": round(tf(f_ms), 1), "fused_mfma_frac": round(tf(f_ms) / MFMA_BF16_PEAK_TFS, 4),
+            "fused_GBs": round(byts / (f_ms * 1e-3) / 1e9, 1),
+            "store_g_control_us": round(g_ms * 1e3, 2), "store_g_control_TFs": round(tf(g_ms), 1),
+            "store_g_control_mfma_frac": round(tf(g_ms) / MFMA_BF16_PEAK_TFS, 4),
+            "timing": "median of 11 batches of 12 back-to-back launches"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None, help="timed steps (default: per workload)")
     ap.add_argument("--warmup", type=int, default=None, help="untimed warmup steps (default: per workload)")
-    ap.add_argument("--workload", default="sweep", choices=["sweep", "o_proj", "mlp", "mlp_i8", "mlp_i8r64"])
+    ap.add_argument("--workload", default="sweep", choices=["sweep", "o_proj", "o_proj_t4096", "mlp", "mlp_i8",
+                                                            "mlp_i8r64"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
     ap.add_argument("--streams", type=int, default=1,
@@ -444,6 +486,7 @@ def main():
         "config": {
             "workload": {"sweep": "Llama-3.1-8B linear-layer sweep: 32 x {q,k,v,o,gate,up,down} + lm_head, T=512, bf16 W/m/v",
                          "o_proj": "Llama-3.1-8B o_proj 4096x4096, T=512, bf16 W/m/v",
+                         "o_proj_t4096": "Llama-3.1-8B o_proj 4096x4096, T=4096, bf16 W/m/v",
                          "mlp": "Llama-3.1-8B gate/up/down, T=512, bf16 W/m/v",
                          "mlp_i8": "Llama-3.1-8B gate/up/down, T=512, int8 m/v (256-row blocks)",
                          "mlp_i8r64": "Llama-3.1-8B gate/up/down, T=512, int8 m/v (64-wide row blocks)"}[args.workload]
@@ -461,6 +504,18 @@ def main():
             "traffic": traffic,
             "kernel": f"{kernel} (forge_linear_step_grouped)",
             "algorithmic_bytes_per_launch": round(fused_b / len(launches)),
+            "avg_launch_us": round(avg_launch_ms * 1e3, 3),
+            "launches_per_step": len(launches),
+        } if not compute_bound(T) else {
+            # past the ridge (T > ~1.9k for bf16 state) the GEMM bounds the step
+            "bound": "mfma",
+            "achieved": round(flops / len(launches) / (avg_launch_ms * 1e-3) / 1e12, 2),
+            "peak": MFMA_BF16_PEAK_TFS,
+            "unit": "TFLOP/s",
+            "frac": round(flops / len(launches) / (avg_launch_ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFS, 4),
+            "traffic": traffic,
+            "kernel": f"{kernel} (forge_linear_step_grouped)",
+            "algorithmic_flops_per_launch": round(flops / len(launches)),
             "avg_launch_us": round(avg_launch_ms * 1e3, 3),
             "launches_per_step": len(launches),
         },
@@ -501,6 +556,9 @@ def main():
         torch.cuda.empty_cache()
         import oracle
         out["configs"] = single_configs(device, oracle.num_threads())
+        log("compute-bound regime: o_proj at T=4096")
+        out["compute_bound"] = compute_bound_block(device)
+        log(f"compute-bound: {out['compute_bound']}")
 
     if not args.no_ceilings:
         mats = launches = None

@@ -11,6 +11,8 @@ activations and gradients):
                  fp32 moments starting at zero, steps 1..3.
 * ``o_proj``     T=512, 4096x4096, X std 1, dY std 1e-3, W std 0.02, bf16 moments from a
                  warm state m~N(0,1e-4), v=|N(0,1e-6)|, step 100.
+* ``o_proj_t4096``  ``o_proj`` at T=4096 tokens, where the GEMM (2T flop per parameter)
+                 outweighs the state traffic: the compute-bound regime.
 * ``mlp``        T=512, gate/up [14336x4096], down [4096x14336], as ``o_proj``.
 * ``mlp_i8``     ``mlp`` with int8 block-absmax moments (256-row column blocks, sqrt(v)).
 * ``mlp_i8r64``  ``mlp`` with int8 moments in 64-wide row blocks (v stored).
@@ -111,6 +113,7 @@ WORKLOADS = {
     "layer256": Workload("layer256", 128, (Matrix("layer256", 256, 256, 0),), "f32",
                          x_std=1.0, dy_std=0.01, m_std=0.0, v_std=0.0, steps=(1, 2, 3)),
     "o_proj": Workload("o_proj", 512, (Matrix("o_proj", 4096, 4096, 2),), "bf16"),
+    "o_proj_t4096": Workload("o_proj_t4096", 4096, (Matrix("o_proj", 4096, 4096, 2),), "bf16"),
     "mlp": Workload("mlp", 512, (Matrix("gate", 14336, 4096, 3), Matrix("up", 14336, 4096, 4),
                                  Matrix("down", 4096, 14336, 5)), "bf16"),
     "mlp_i8": Workload("mlp_i8", 512, (Matrix("gate", 14336, 4096, 6), Matrix("up", 14336, 4096, 7),

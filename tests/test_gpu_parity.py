@@ -111,6 +111,12 @@ def test_o_proj_full():
     _full_matrix("o_proj", 0)
 
 
+def test_o_proj_t4096_full():
+    """Every element of the o_proj shape at T = 4096 (128 token chunks per tile), the
+    compute-bound regime that bench.py times beside the sweep."""
+    _full_matrix("o_proj_t4096", 0)
+
+
 @pytest.mark.parametrize("idx", [0, 1, 2], ids=["gate", "up", "down"])
 def test_mlp_bf16_full(idx):
     _full_matrix("mlp", idx)
