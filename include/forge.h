@@ -388,12 +388,15 @@ FORGE_API forge_status forge_linear_step_unfused_noalloc(const void *X, const vo
 FORGE_API const char *forge_status_string(int32_t status);
 
 /*
- * forge_query_tile -- the tile geometry the fused kernel uses for `moment_dtype`:
- * rows of W (along d_out), columns (along d_in) and tokens per pipeline chunk.
- * Any output pointer may be NULL.  Returns FORGE_ERR_INVALID_DTYPE for an unknown code.
+ * forge_query_tile -- the tile geometry that the fused step uses on a matrix W [d_out, d_in]
+ * with T tokens and `moment_dtype` state: rows of W (along d_out), columns (along d_in) and
+ * tokens per pipeline chunk.  The fixed counterpart of App. H's per-shape tile choice:
+ * 256x64 for int8 moments in 256-row blocks (one scale block per tile), 128x128 for every
+ * other kind, at every shape.  Any output pointer may be NULL.  Returns
+ * FORGE_ERR_INVALID_DTYPE for an unknown code and FORGE_ERR_INVALID_SHAPE for a negative size.
  */
-FORGE_API forge_status forge_query_tile(int32_t moment_dtype, int32_t *tile_rows, int32_t *tile_cols,
-                              int32_t *tile_tokens);
+FORGE_API forge_status forge_query_tile(int64_t T, int64_t d_in, int64_t d_out, int32_t moment_dtype,
+                                        int32_t *tile_rows, int32_t *tile_cols, int32_t *tile_tokens);
 
 #ifdef __cplusplus
 }

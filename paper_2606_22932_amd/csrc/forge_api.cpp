@@ -383,10 +383,12 @@ const char *forge_status_string(int32_t s)
     }
 }
 
-forge_status forge_query_tile(int32_t md, int32_t *rows, int32_t *cols, int32_t *tokens)
+forge_status forge_query_tile(int64_t T, int64_t d_in, int64_t d_out, int32_t md, int32_t *rows,
+                              int32_t *cols, int32_t *tokens)
 {
     if (check_dtype_moment(md) != FORGE_OK) return FORGE_ERR_INVALID_DTYPE;
-    const forge_impl::TileShape t = forge_impl::tile_shape(md);
+    if (T < 0 || d_in < 0 || d_out < 0) return FORGE_ERR_INVALID_SHAPE;
+    const forge_impl::TileShape t = forge_impl::tile_shape(md);   // one tile per moment kind, any shape
     if (rows) *rows = t.rows;
     if (cols) *cols = t.cols;
     if (tokens) *tokens = t.tokens;

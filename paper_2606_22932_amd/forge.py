@@ -82,7 +82,8 @@ _SIGS = {
     "forge_linear_step_unfused_noalloc": [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I32, _F, _F, _F, _F,
                                           _F, _I64, _I32, _P],
     "forge_status_string": [_I32],
-    "forge_query_tile": [_I32, ctypes.POINTER(_I32), ctypes.POINTER(_I32), ctypes.POINTER(_I32)],
+    "forge_query_tile": [_I64, _I64, _I64, _I32, ctypes.POINTER(_I32), ctypes.POINTER(_I32),
+                         ctypes.POINTER(_I32)],
 }
 
 
@@ -115,9 +116,10 @@ def forge_status_string(code: int) -> str:
     return lib().forge_status_string(int(code)).decode()
 
 
-def forge_query_tile(moment_dtype: int):
+def forge_query_tile(T: int, d_in: int, d_out: int, moment_dtype: int):
     r, c, t = _I32(), _I32(), _I32()
-    st = lib().forge_query_tile(int(moment_dtype), ctypes.byref(r), ctypes.byref(c), ctypes.byref(t))
+    st = lib().forge_query_tile(int(T), int(d_in), int(d_out), int(moment_dtype), ctypes.byref(r),
+                                ctypes.byref(c), ctypes.byref(t))
     _check(st, "forge_query_tile")
     return r.value, c.value, t.value
 

@@ -61,12 +61,15 @@ def test_status_strings():
 
 
 def test_query_tile():
-    assert forge.forge_query_tile(BF16)[0] % 8 == 0
-    rows, cols, tk = forge.forge_query_tile(I8)
+    assert forge.forge_query_tile(512, 4096, 4096, BF16) == (128, 128, 32)
+    assert forge.forge_query_tile(4096, 4096, 4096, BF16) == (128, 128, 32)   # one tile at every T
+    rows, cols, tk = forge.forge_query_tile(512, 4096, 14336, I8)
     assert rows == 256            # an int8 tile is exactly one scale block tall
-    assert forge.forge_query_tile(3)[1] % 64 == 0   # row-block int8: whole 64-wide blocks per tile
+    assert forge.forge_query_tile(512, 4096, 4096, 3)[1] % 64 == 0   # row-block int8: whole 64-wide blocks
     r = ctypes.c_int32()
-    assert lib().forge_query_tile(7, ctypes.byref(r), None, None) == DTYPE
+    assert lib().forge_query_tile(512, 64, 64, 7, ctypes.byref(r), None, None) == DTYPE
+    assert lib().forge_query_tile(-1, 64, 64, BF16, ctypes.byref(r), None, None) == SHAPE
+    assert lib().forge_query_tile(512, 64, -8, BF16, None, None, None) == SHAPE
 
 
 def test_dtype_errors():
