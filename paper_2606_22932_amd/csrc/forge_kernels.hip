@@ -477,20 +477,20 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_of(const void *base, uint
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)n, 0x00020000);
 }
 
-template <int BP, int BQ, int MK, int E>
+template <int BP, int BQ, int MK, int E, int AH = 0>
 struct EpiRule {
     using M = EpiMap<BP, BQ>;
     using R = Rule<E>;
     static constexpr bool PREFETCH = (MK == MK_BF16);
     static constexpr int NPF = PREFETCH ? M::NPASS : 1;
-    // Row passes whose state is loaded while the mainloop runs; the loads of the others are
-    // issued as the epilogue starts, AHEAD passes before their use.  With all eight passes
-    // in flight at a workgroup's start the sweep ran 1.1 % slower (less state in flight
-    // per CU suits in-place HBM traffic; fewer than six loses overlap with the GEMM).
+    // Row passes whose state is loaded while the mainloop runs (AH, or by default all but
+    // two); the loads of the others are issued as the epilogue starts, AHEAD passes before
+    // their use.  Less state in flight per CU suits in-place HBM traffic, fewer than six
+    // passes loses overlap with the GEMM; the launcher picks all eight for long launches.
 #ifdef FORGE_PF_AHEAD
     static constexpr int AHEAD = FORGE_PF_AHEAD < M::NPASS ? FORGE_PF_AHEAD : M::NPASS;
 #else
-    static constexpr int AHEAD = M::NPASS > 2 ? M::NPASS - 2 : M::NPASS;
+    static constexpr int AHEAD = AH > 0 ? (AH < M::NPASS ? AH : M::NPASS) : (M::NPASS > 2 ? M::NPASS - 2 : M::NPASS);
 #endif
     u32x4_t pw[R::W_RW ? NPF : 1], ps1[R::NS >= 1 ? NPF : 1], ps2[R::NS >= 2 ? NPF : 1];
 
@@ -967,7 +967,7 @@ template <int BP, int BQ, bool W, bool M> struct IsEpiQ<EpiQ<BP, BQ, W, M>> { st
 
 // The epilogue of (moment kind, rule): the row-block int8 layout and the fp8 encodings have
 // their own (AdamW only).
-template <int BP, int BQ, int MK, int E> struct EpiSel { using T = EpiRule<BP, BQ, MK, E>; };
+template <int BP, int BQ, int MK, int E, int AH = 0> struct EpiSel { using T = EpiRule<BP, BQ, MK, E, AH>; };
 template <int BP, int BQ> struct EpiSel<BP, BQ, MK_I8R64, EPI_ADAMW> { using T = EpiI8Row<BP, BQ>; };
 template <int BP, int BQ> struct EpiSel<BP, BQ, MK_FP8, EPI_ADAMW> { using T = EpiQ<BP, BQ, false, true>; };
 template <int BP, int BQ> struct EpiSel<BP, BQ, MK_BF16, EPI_ADAMW_WFP8> { using T = EpiQ<BP, BQ, true, false>; };
@@ -1193,7 +1193,7 @@ __device__ __forceinline__ void epi_store_g(const Args &a, int p0, int q0, int s
 
 // At most 128 VGPRs (four waves per SIMD): two 512-thread workgroups per CU, one math and
 // one stream wave of each on every SIMD.  At 129-136 registers only one would fit.
-template <int BP, int BQ, int MK, int EPI>
+template <int BP, int BQ, int MK, int EPI, int AH = 0>
 __global__ void __launch_bounds__(NT, 4) fused_kernel(GroupArgs g)
 {
     static_assert(MK != MK_I8, "int8 moments run in pipelined_i8_kernel");
@@ -1227,7 +1227,7 @@ __global__ void __launch_bounds__(NT, 4) fused_kernel(GroupArgs g)
         ml.template stage_g<EM::GP>(Gs, wave, lane);
         lds_barrier();
     } else if constexpr (EPI != EPI_STORE_BF16 && EPI != EPI_STORE_F32) {
-        typename EpiSel<BP, BQ, MK, EPI>::T ep;
+        typename EpiSel<BP, BQ, MK, EPI, AH>::T ep;
         if constexpr (IsEpiQ<decltype(ep)>::value) ep.first_tile = (t == g.start[mi]);
         ep.prefetch(a, p0, q0, s);
         for (int i = 0; i < nbar; ++i) lds_barrier();
@@ -1710,6 +1710,16 @@ static hipError_t launch_group(const Args *a, int n, hipStream_t st)
         g.start[i + 1] = g.start[n];
     }
     if (g.start[n] == 0) return hipSuccess;
+    // Prefetch depth by launch length (AdamW on bf16 state): a launch of at least 8 waves of
+    // resident tiles loads all eight row passes of a tile's state during its mainloop, a
+    // shorter one six.  Measured per launch group of the Llama-3.1-8B sweep at T = 512:
+    // lm_head (63 waves) 1157 against 1222 us, gate+up (14) even, down (7), o (2) and
+    // q+k+v (3) 1-7 % slower with eight.
+    if constexpr (MK == MK_BF16 && EPI == EPI_ADAMW)
+        if (g.start[n] >= 8 * 2 * device_cu_count()) {
+            hipLaunchKernelGGL((fused_kernel<BP, BQ, MK, EPI, 8>), dim3(g.start[n]), dim3(NT), 0, st, g);
+            return hipGetLastError();
+        }
     hipLaunchKernelGGL((fused_kernel<BP, BQ, MK, EPI>), dim3(g.start[n]), dim3(NT), 0, st, g);
     return hipGetLastError();
 }

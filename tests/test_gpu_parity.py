@@ -264,6 +264,33 @@ def test_grouped_shared_input_and_empty_member():
         _say(check_step(dict(W=bits(W), m=bits(m), v=bits(v)), run_oracle(p, 7), "bf16", hp=p.hp))
 
 
+def test_long_launch_prefetch_depth_bitwise():
+    """A launch of at least 8 waves of resident tiles (4096 tiles of 128x128 on 256 CUs)
+    prefetches all eight row passes of a tile's state, a shorter one six.  The depth changes
+    when loads are issued, not what is computed: four o_proj-sized matrices in one grouped
+    launch (4096 tiles) give the bits of four single launches (1024 tiles each), and the
+    first is checked against the oracle on every element."""
+    T, d = 512, 4096
+    probs = [make_problem(T, d, d, "bf16", seed=70 + k) for k in range(4)]
+    _say(f"long launch: 4 x {d}x{d}, T={T}")
+    group, single = [], []
+    for p in probs:
+        X, dY = dev(p.X), dev(p.dY)
+        W, m, v, _, _ = _state_on_gpu(p)
+        group.append((X, dY, W, m, v))
+        W2, m2, v2, _, _ = _state_on_gpu(p)
+        forge.forge_linear_step(X, dY, W2, m2, v2, step=100, **p.hp)
+        single.append((W2, m2, v2))
+    forge.forge_linear_step_grouped(group, step=100, **probs[0].hp)
+    torch.cuda.synchronize()
+    for g, s1 in zip(group, single):
+        for a, b in zip(g[2:], s1):
+            assert torch.equal(a.view(torch.uint8), b.view(torch.uint8)), "long launch != short launches"
+    g = group[0]
+    _say(check_step(dict(W=bits(g[2]), m=bits(g[3]), v=bits(g[4])), run_oracle(probs[0], 100), "bf16",
+                    hp=probs[0].hp))
+
+
 @pytest.mark.parametrize("shape", [(512, 520, 776), (77, 328, 264), (0, 64, 256)], ids=lambda s: "x".join(map(str, s)))
 def test_int8_fused_equals_unfused_fp32_gradient_bitwise(shape):
     """The fused int8 step and the two-kernel step through an fp32 G accumulate every
