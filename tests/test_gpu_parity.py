@@ -340,3 +340,43 @@ def test_int8_exact_ties_round_half_even(moment):
     got = gpu["m"][:n, :] if moment == "i8" else gpu["m"][:, :n].T
     assert (got == np.array(TIE_CODES_EVEN)[:, None]).all()
     assert (gpu["m_scale"] == 1.0).all()
+
+
+# The fused bf16 step (one workgroup per 128x128 tile, two resident per CU) against the
+# two-kernel path (the store-G GEMM, then the stand-alone optimizer).  Shapes: fewer tiles
+# than CUs, ragged edges on both axes, ragged token chunks, the empty token axis, and the
+# o_proj shape (1024 tiles, two waves of resident workgroups).
+BITWISE = [(512, 520, 776), (77, 1032, 2056), (33, 8, 8), (0, 264, 1032), (1024, 520, 392),
+           (512, 4096, 4096)]
+
+
+@pytest.mark.parametrize("shape", BITWISE, ids=lambda s: "x".join(map(str, s)))
+def test_bf16_fused_equals_unfused_fp32_gradient_bitwise(shape):
+    """The fused bf16 step and the two-kernel step through an fp32 G accumulate every
+    element of G in the same order and share the AdamW arithmetic: identical bits."""
+    T, d_in, d_out = shape
+    p = make_problem(T, d_in, d_out, "bf16", seed=91 + T)
+    _say(f"fused vs unfused: T={T} d_in={d_in} d_out={d_out}")
+    a = run_gpu(p, 100)
+    b = run_gpu(p, 100, path="unfused", grad="f32")
+    for k in ("W", "m", "v"):
+        assert np.array_equal(a[k].view(np.uint8), b[k].view(np.uint8)), k
+
+
+def test_bf16_grouped_mixed_shapes_bitwise():
+    """A grouped launch of matrices of different shapes gives the bits of the matrices
+    stepped one by one through the two-kernel path."""
+    T = 300
+    shapes = [(T, 264, 136), (T, 1032, 520), (T, 128, 8), (T, 520, 1160)]
+    probs = [make_problem(*s, "bf16", seed=140 + k) for k, s in enumerate(shapes)]
+    group = []
+    for p in probs:
+        X, dY = dev(p.X), dev(p.dY)
+        W, m, v, _, _ = _state_on_gpu(p)
+        group.append((X, dY, W, m, v))
+    forge.forge_linear_step_grouped(group, step=100, **probs[0].hp)
+    torch.cuda.synchronize()
+    for g, p in zip(group, probs):
+        b = run_gpu(p, 100, path="unfused", grad="f32")
+        for k, t in zip(("W", "m", "v"), g[2:]):
+            assert np.array_equal(bits(t).view(np.uint8), b[k].view(np.uint8)), k
