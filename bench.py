@@ -34,28 +34,28 @@ COPY_BYTES = 1 << 30           # size of the calibration copy (--copy-calibratio
 # sources whose sha256 is recorded: after any change to them the figure is reported as null.
 TRAFFIC = {
     "sweep": {
-        "source_sha256": "21b32061fcb0175866119c4f05eeaedec9b4e9ac242d30994ba693a73f1c3964",
-        "fetch_kib_per_launch": 206223.0,     # FETCH_SIZE, mean over the 129 launches of a step
-        "write_kib_per_launch": 340884.4,     # WRITE_SIZE
+        "source_sha256": "a02c4c42687392f8a41d58b14a1a96bf37ff628c801dec4ba4a2f4b1083e9533",
+        "fetch_kib_per_launch": 207207.1,     # FETCH_SIZE, mean over the 129 launches of a step
+        "write_kib_per_launch": 340878.4,     # WRITE_SIZE
         "fetch_scale": 1.99992,               # 1 GiB copy: FETCH_SIZE reads 524308 KiB
         "write_scale": 1.0,                   # 1 GiB copy: WRITE_SIZE reads 1048576 KiB
-        "bytes_per_launch": 771394305,        # (fetch * fetch_scale + write * write_scale) KiB
+        "bytes_per_launch": 773402602,        # (fetch * fetch_scale + write * write_scale) KiB
     },
     "mlp_i8": {
-        "source_sha256": "21b32061fcb0175866119c4f05eeaedec9b4e9ac242d30994ba693a73f1c3964",
-        "fetch_kib_per_launch": 153636.2,     # mean over the 3 launches (gate, up, down)
-        "write_kib_per_launch": 262406.3,
+        "source_sha256": "a02c4c42687392f8a41d58b14a1a96bf37ff628c801dec4ba4a2f4b1083e9533",
+        "fetch_kib_per_launch": 153183.6,     # mean over the 3 launches (gate, up, down)
+        "write_kib_per_launch": 263087.4,
         "fetch_scale": 1.99992,
         "write_scale": 1.0,
-        "bytes_per_launch": 583338663,
+        "bytes_per_launch": 583109499,
     },
     "mlp_i8r64": {
-        "source_sha256": "21b32061fcb0175866119c4f05eeaedec9b4e9ac242d30994ba693a73f1c3964",
-        "fetch_kib_per_launch": 155836.6,     # mean over the 3 launches (gate, up, down)
-        "write_kib_per_launch": 239203.4,
+        "source_sha256": "a02c4c42687392f8a41d58b14a1a96bf37ff628c801dec4ba4a2f4b1083e9533",
+        "fetch_kib_per_launch": 155846.7,     # mean over the 3 launches (gate, up, down)
+        "write_kib_per_launch": 239245.6,
         "fetch_scale": 1.99992,
         "write_scale": 1.0,
-        "bytes_per_launch": 564085583,
+        "bytes_per_launch": 564149399,
     },
 }
 
