@@ -34,28 +34,52 @@ COPY_BYTES = 1 << 30           # size of the calibration copy (--copy-calibratio
 # sources whose sha256 is recorded: after any change to them the figure is reported as null.
 TRAFFIC = {
     "sweep": {
-        "source_sha256": "a02c4c42687392f8a41d58b14a1a96bf37ff628c801dec4ba4a2f4b1083e9533",
-        "fetch_kib_per_launch": 207207.1,     # FETCH_SIZE, mean over the 129 launches of a step
-        "write_kib_per_launch": 340878.4,     # WRITE_SIZE
-        "fetch_scale": 1.99992,               # 1 GiB copy: FETCH_SIZE reads 524308 KiB
+        "source_sha256": "6c78cc33ad527443c89a0478d176d1f6d0ef62b09111bbf55d2565fbd8ca542d",
+        "fetch_kib_per_launch": 209017.3,     # FETCH_SIZE, mean over the 129 launches of a step
+        "write_kib_per_launch": 340883.2,     # WRITE_SIZE
+        "fetch_scale": 1.99992,               # 1 GiB copy: FETCH_SIZE reads about 524300 KiB
         "write_scale": 1.0,                   # 1 GiB copy: WRITE_SIZE reads 1048576 KiB
-        "bytes_per_launch": 773402602,        # (fetch * fetch_scale + write * write_scale) KiB
+        "bytes_per_launch": 777115590,        # (fetch * fetch_scale + write * write_scale) KiB
     },
     "mlp_i8": {
-        "source_sha256": "a02c4c42687392f8a41d58b14a1a96bf37ff628c801dec4ba4a2f4b1083e9533",
-        "fetch_kib_per_launch": 153183.6,     # mean over the 3 launches (gate, up, down)
-        "write_kib_per_launch": 263087.4,
-        "fetch_scale": 1.99992,
+        "source_sha256": "6c78cc33ad527443c89a0478d176d1f6d0ef62b09111bbf55d2565fbd8ca542d",
+        "fetch_kib_per_launch": 152790.6,     # mean over the 3 launches (gate, up, down)
+        "write_kib_per_launch": 262457.9,
+        "fetch_scale": 1.99989,
         "write_scale": 1.0,
-        "bytes_per_launch": 583109499,
+        "bytes_per_launch": 581655497,
     },
     "mlp_i8r64": {
-        "source_sha256": "a02c4c42687392f8a41d58b14a1a96bf37ff628c801dec4ba4a2f4b1083e9533",
-        "fetch_kib_per_launch": 155846.7,     # mean over the 3 launches (gate, up, down)
-        "write_kib_per_launch": 239245.6,
+        "source_sha256": "6c78cc33ad527443c89a0478d176d1f6d0ef62b09111bbf55d2565fbd8ca542d",
+        "fetch_kib_per_launch": 155854.9,     # mean over the 3 launches (gate, up, down)
+        "write_kib_per_launch": 240778.8,
         "fetch_scale": 1.99992,
         "write_scale": 1.0,
-        "bytes_per_launch": 564149399,
+        "bytes_per_launch": 565736070,
+    },
+    "mlp_fp8": {
+        "source_sha256": "6c78cc33ad527443c89a0478d176d1f6d0ef62b09111bbf55d2565fbd8ca542d",
+        "fetch_kib_per_launch": 147132.5,     # mean over the 3 launches (gate, up, down)
+        "write_kib_per_launch": 229395.3,
+        "fetch_scale": 1.99993,
+        "write_scale": 1.0,
+        "bytes_per_launch": 536216860,
+    },
+    "mlp_wfp8": {
+        "source_sha256": "6c78cc33ad527443c89a0478d176d1f6d0ef62b09111bbf55d2565fbd8ca542d",
+        "fetch_kib_per_launch": 178042.5,     # mean over the 3 launches (gate, up, down)
+        "write_kib_per_launch": 286730.1,
+        "fetch_scale": 1.99992,
+        "write_scale": 1.0,
+        "bytes_per_launch": 658228770,
+    },
+    "mlp_wfp8_fp8": {
+        "source_sha256": "6c78cc33ad527443c89a0478d176d1f6d0ef62b09111bbf55d2565fbd8ca542d",
+        "fetch_kib_per_launch": 116025.8,     # mean over the 3 launches (gate, up, down)
+        "write_kib_per_launch": 172061.6,
+        "fetch_scale": 1.99992,
+        "write_scale": 1.0,
+        "bytes_per_launch": 413802564,
     },
 }
 
@@ -64,7 +88,8 @@ TRAFFIC = {
 # sweep's 20 ms steps need few; the single-matrix and MLP workloads get enough steps for
 # about 0.1 s of warmup and 0.2 s of timed work, so that clocks and TLBs are warm.
 DEFAULT_STEPS = {"sweep": (3, 10), "o_proj": (2000, 4000), "o_proj_t4096": (300, 600), "mlp": (200, 400),
-                 "mlp_i8": (200, 300), "mlp_i8r64": (200, 400)}
+                 "mlp_i8": (200, 300), "mlp_i8r64": (200, 400), "mlp_fp8": (200, 400), "mlp_wfp8": (200, 400),
+                 "mlp_wfp8_fp8": (200, 400)}
 
 
 def log(*a):
@@ -83,6 +108,13 @@ def build_workload(wl, device, moment_override=None):
             mq, vq, ms, vs = synth.random_i8_state(mat, wl, device=device,
                                                    layout="col256" if wl.moment == "i8" else "row64")
             mats.append(dict(mat=mat, X=X, dY=dY, W=W, m=mq, v=vq, ms=ms, vs=vs))
+        elif wl.moment == "fp8" or wl.weight == "fp8":
+            W8, w_ring, m8, m_ring, v8, v_ring = synth.random_fp8_state(mat, wl, device=device)
+            if W8 is not None:
+                W = W8
+            if m8 is None:
+                m8, v8 = synth.warm_moments(mat, wl, device=device, dtype=torch.bfloat16)
+            mats.append(dict(mat=mat, X=X, dY=dY, W=W, w_ring=w_ring, m=m8, v=v8, ms=m_ring, vs=v_ring))
         else:
             dt = torch.bfloat16 if wl.moment == "bf16" else torch.float32
             m, v = synth.warm_moments(mat, wl, device=device, dtype=dt)
@@ -373,13 +405,56 @@ def compute_bound_block(device):
             "timing": "median of 11 batches of 12 back-to-back launches"}
 
 
+# The other state encodings, on the MLP projections at T = 512 (C3's shapes): int8 moments
+# in 64-wide row blocks (the paper's own int8 layout), fp8 E4M3 moments, fp8 E4M3 weights
+# with bf16 moments, and both.  Each is timed like C3 and C4 (one launch per matrix).
+ENCODINGS = ("mlp_i8r64", "mlp_fp8", "mlp_wfp8", "mlp_wfp8_fp8")
+
+
+def encodings_block(device):
+    import torch
+    from paper_2606_22932_amd import accounting, forge, synth
+    out = {}
+    for name in ENCODINGS:
+        wl = synth.WORKLOADS[name]
+        hp = wl.hyper
+        mats = build_workload(wl, device)
+        torch.cuda.synchronize()
+
+        def launch(d, k):
+            if wl.weight == "fp8":
+                forge.forge_linear_step_wfp8(d["X"], d["dY"], d["W"], d["w_ring"], d["m"], d["v"], d["ms"], d["vs"],
+                                             step=wl.steps[0], **hp)
+            else:
+                forge.forge_linear_step(d["X"], d["dY"], d["W"], d["m"], d["v"], d["ms"], d["vs"],
+                                        step=wl.steps[0], **hp)
+
+        us, lo, hi = 0.0, 0.0, 0.0
+        for d in mats:
+            med, a, b = time_batches([d], launch, 10, 21, 30)
+            us, lo, hi = us + med * 1e3, lo + a * 1e3, hi + b * 1e3
+        byts = sum(accounting.fused_bytes(wl.T, m_.d_in, m_.d_out, wl.moment, wl.weight) for m_ in wl.matrices)
+        gbs = byts / (us * 1e-6) / 1e9
+        tr = measured_traffic(name)
+        out[name] = {"weights": wl.weight, "moments": wl.moment,
+                     "state_bytes_per_param": accounting.state_bytes_per_param(wl.moment, wl.weight),
+                     "algorithmic_bytes": byts, "gpu_us": round(us, 2), "gpu_us_range": [round(lo, 2), round(hi, 2)],
+                     "gpu_GBs": round(gbs, 1), "frac_of_8TBs": round(gbs / HBM_PEAK_GBS, 4),
+                     "traffic_over_algorithmic": None if tr is None else
+                     round(tr["bytes_per_launch"] * len(wl.matrices) / byts, 4)}
+        del mats
+        torch.cuda.empty_cache()
+    out["timing"] = "sum over gate, up, down of the median of 21 batches of 10 back-to-back launches"
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None, help="timed steps (default: per workload)")
     ap.add_argument("--warmup", type=int, default=None, help="untimed warmup steps (default: per workload)")
     ap.add_argument("--workload", default="sweep", choices=["sweep", "o_proj", "o_proj_t4096", "mlp", "mlp_i8",
-                                                            "mlp_i8r64"])
+                                                            "mlp_i8r64", "mlp_fp8", "mlp_wfp8", "mlp_wfp8_fp8"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
     ap.add_argument("--streams", type=int, default=1,
@@ -453,10 +528,15 @@ def main():
     def fused(group, t):
         st = streams[nlaunch[0] % len(streams)]
         nlaunch[0] += 1
+        if wl.weight == "fp8":
+            for d in group:
+                forge.forge_linear_step_wfp8(d["X"], d["dY"], d["W"], d["w_ring"], d["m"], d["v"], d["ms"], d["vs"],
+                                             step=t, stream=st.cuda_stream, **hp)
+            return
         forge.forge_linear_step_grouped([(d["X"], d["dY"], d["W"], d["m"], d["v"], d["ms"], d["vs"])
                                          for d in group], step=t, stream=st.cuda_stream, **hp)
 
-    fused_b = sum(accounting.fused_bytes(T, d["mat"].d_in, d["mat"].d_out, wl.moment) for d in mats)
+    fused_b = sum(accounting.fused_bytes(T, d["mat"].d_in, d["mat"].d_out, wl.moment, wl.weight) for d in mats)
     flops = sum(accounting.gemm_flops(T, d["mat"].d_in, d["mat"].d_out) for d in mats)
     log(f"timing fused ({len(launches)} launches per step)")
     total, wall = time_steps(launches, wl, fused, args.steps, args.warmup, wl.steps[0], streams[1:])
@@ -470,6 +550,7 @@ def main():
     tr = measured_traffic(args.workload) if args.tokens is None else None   # measured at the workload's T
     traffic = None if tr is None else tr["bytes_per_launch"]
     kernel = "pipelined_i8_kernel" if wl.moment == "i8" else "fused_kernel"
+    entry = "forge_linear_step_wfp8" if wl.weight == "fp8" else "forge_linear_step_grouped"
     out = {
         "metric": "fused dW+AdamW step: HBM GB/s & % roofline; ms per Llama-8B linear sweep",
         "value": round(value, 2),
@@ -489,11 +570,14 @@ def main():
                          "o_proj_t4096": "Llama-3.1-8B o_proj 4096x4096, T=4096, bf16 W/m/v",
                          "mlp": "Llama-3.1-8B gate/up/down, T=512, bf16 W/m/v",
                          "mlp_i8": "Llama-3.1-8B gate/up/down, T=512, int8 m/v (256-row blocks)",
-                         "mlp_i8r64": "Llama-3.1-8B gate/up/down, T=512, int8 m/v (64-wide row blocks)"}[args.workload]
+                         "mlp_i8r64": "Llama-3.1-8B gate/up/down, T=512, int8 m/v (64-wide row blocks)",
+                         "mlp_fp8": "Llama-3.1-8B gate/up/down, T=512, bf16 W, fp8 E4M3 m and sqrt(v)",
+                         "mlp_wfp8": "Llama-3.1-8B gate/up/down, T=512, fp8 E4M3 W, bf16 m/v",
+                         "mlp_wfp8_fp8": "Llama-3.1-8B gate/up/down, T=512, fp8 E4M3 W, m and sqrt(v)"}[args.workload]
                         .replace("T=512", f"T={T}"),
             "T": T, "matrices": len(mats),
             "params": sum(d["mat"].d_in * d["mat"].d_out for d in mats),
-            "moments": wl.moment, "algorithmic_bytes_per_step": fused_b,
+            "moments": wl.moment, "weights": wl.weight, "algorithmic_bytes_per_step": fused_b,
         },
         "roofline": {
             "bound": "hbm",
@@ -502,7 +586,7 @@ def main():
             "unit": "GB/s",
             "frac": round(kern_gbs / HBM_PEAK_GBS, 4),
             "traffic": traffic,
-            "kernel": f"{kernel} (forge_linear_step_grouped)",
+            "kernel": f"{kernel} ({entry})",
             "algorithmic_bytes_per_launch": round(fused_b / len(launches)),
             "avg_launch_us": round(avg_launch_ms * 1e3, 3),
             "launches_per_step": len(launches),
@@ -514,7 +598,7 @@ def main():
             "unit": "TFLOP/s",
             "frac": round(flops / len(launches) / (avg_launch_ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFS, 4),
             "traffic": traffic,
-            "kernel": f"{kernel} (forge_linear_step_grouped)",
+            "kernel": f"{kernel} ({entry})",
             "algorithmic_flops_per_launch": round(flops / len(launches)),
             "avg_launch_us": round(avg_launch_ms * 1e3, 3),
             "launches_per_step": len(launches),
@@ -523,7 +607,7 @@ def main():
         "mfma_frac": round(flops / (ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFS, 4),
     }
 
-    if not args.no_unfused and wl.moment != "f32":
+    if not args.no_unfused and wl.moment not in ("f32", "fp8") and wl.weight == "bf16":
         biggest = max(d["mat"].d_in * d["mat"].d_out for d in mats)
         G_ws = torch.empty(biggest, dtype=torch.bfloat16, device=device)
 
@@ -559,6 +643,9 @@ def main():
         log("compute-bound regime: o_proj at T=4096")
         out["compute_bound"] = compute_bound_block(device)
         log(f"compute-bound: {out['compute_bound']}")
+        log("state encodings on the MLP projections")
+        out["encodings"] = encodings_block(device)
+        log(f"encodings: {out['encodings']}")
 
     if not args.no_ceilings:
         mats = launches = None

@@ -277,17 +277,21 @@ struct Mainloop {
         }
     }
 
-    // The whole token loop; executes exactly nbar(T) workgroup barriers.
+    // The whole token loop; executes exactly nbar(T) workgroup barriers.  The first follows
+    // the DMA of the first NS-1 chunks: a workgroup's other waves issue their own global
+    // loads (the tile's state) after it, so these chunks are queued ahead of them in the
+    // CU's vector memory path.
     __device__ __forceinline__ void run(const Args &a, int p0, int q0, unsigned char *lds, int wave,
                                         int lane)
     {
         begin(a, p0, q0, lds, wave, lane);
+        lds_barrier();
         body(a, lds, wave);
         lds_barrier();   // every wave is done reading the stages, which G reuses
     }
 
     static __device__ __forceinline__ int nch(int T) { return (T + TK - 1) / TK; }
-    static __device__ __forceinline__ int nbar(int T) { return (T + TK - 1) / TK + 1; }
+    static __device__ __forceinline__ int nbar(int T) { return (T + TK - 1) / TK + 2; }
 
     // Accumulators -> LDS as G[p][q] (fp32, row pitch GP floats).
     template <int GP>
@@ -1229,8 +1233,16 @@ __global__ void __launch_bounds__(NT, 4) fused_kernel(GroupArgs g)
     } else if constexpr (EPI != EPI_STORE_BF16 && EPI != EPI_STORE_F32) {
         typename EpiSel<BP, BQ, MK, EPI, AH>::T ep;
         if constexpr (IsEpiQ<decltype(ep)>::value) ep.first_tile = (t == g.start[mi]);
+        // The state prefetch leaves after the mainloop's first barrier (its first chunks'
+        // DMA is then ahead of it); for the int8 row-block state, after the barriers of two
+        // more chunks.  Measured at T = 512: the Llama-3.1-8B sweep 19.54-19.55 against
+        // 19.66 ms with the prefetch issued as the workgroup starts, the MLP with int8 row
+        // blocks 0.430 against 0.438 ms; later issue was slower for bf16 state.
+        constexpr int PF_AT = MK == MK_I8R64 ? 3 : 1;
+        int done = 0;
+        for (; done < PF_AT && done < nbar; ++done) lds_barrier();
         ep.prefetch(a, p0, q0, s);
-        for (int i = 0; i < nbar; ++i) lds_barrier();
+        for (; done < nbar; ++done) lds_barrier();
         lds_barrier();
         ep.run(a, p0, q0, s, Gs);
     } else {

@@ -16,6 +16,8 @@ activations and gradients):
 * ``mlp``        T=512, gate/up [14336x4096], down [4096x14336], as ``o_proj``.
 * ``mlp_i8``     ``mlp`` with int8 block-absmax moments (256-row column blocks, sqrt(v)).
 * ``mlp_i8r64``  ``mlp`` with int8 moments in 64-wide row blocks (v stored).
+* ``mlp_fp8``, ``mlp_wfp8``, ``mlp_wfp8_fp8``  ``mlp`` with fp8 E4M3 moments (m and sqrt(v)),
+                 fp8 E4M3 weights with bf16 moments, and both (per-tensor delayed scales).
 * ``sweep``      32 decoder layers x {q,k,v,o,gate,up,down} + lm_head [128256x4096], bf16 moments.
 
 "N(0, s)" means standard deviation s.  Per-tensor seeds are ``1000*base + id`` with ids
@@ -59,13 +61,14 @@ class Workload:
     name: str
     T: int
     matrices: tuple
-    moment: str                  # "f32" | "bf16" | "i8" | "i8r64"
+    moment: str                  # "f32" | "bf16" | "i8" | "i8r64" | "fp8"
     x_std: float = 1.0
     dy_std: float = 1e-3
     w_std: float = 0.02
     m_std: float = 1e-4          # warm first moment (0 -> cold start at zero)
     v_std: float = 1e-6          # warm second moment |N(0, v_std)|
     steps: tuple = (100,)
+    weight: str = "bf16"         # "bf16" | "fp8"
     hyper: dict = field(default_factory=lambda: dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8,
                                                      weight_decay=0.1))
 
@@ -120,6 +123,12 @@ WORKLOADS = {
                                        Matrix("down", 4096, 14336, 8)), "i8"),
     "mlp_i8r64": Workload("mlp_i8r64", 512, (Matrix("gate", 14336, 4096, 6), Matrix("up", 14336, 4096, 7),
                                              Matrix("down", 4096, 14336, 8)), "i8r64"),
+    "mlp_fp8": Workload("mlp_fp8", 512, (Matrix("gate", 14336, 4096, 6), Matrix("up", 14336, 4096, 7),
+                                         Matrix("down", 4096, 14336, 8)), "fp8"),
+    "mlp_wfp8": Workload("mlp_wfp8", 512, (Matrix("gate", 14336, 4096, 6), Matrix("up", 14336, 4096, 7),
+                                           Matrix("down", 4096, 14336, 8)), "bf16", weight="fp8"),
+    "mlp_wfp8_fp8": Workload("mlp_wfp8_fp8", 512, (Matrix("gate", 14336, 4096, 6), Matrix("up", 14336, 4096, 7),
+                                                   Matrix("down", 4096, 14336, 8)), "fp8", weight="fp8"),
     "sweep": Workload("sweep", 512, _sweep_matrices(), "bf16"),
 }
 
@@ -169,6 +178,35 @@ def random_i8_state(mat: Matrix, wl: Workload, device="cpu", layout="col256"):
     ms = torch.full(sshape, wl.m_std * 3 / 127, device=device, dtype=torch.float32)
     vs = torch.full(sshape, v_scale, device=device, dtype=torch.float32)
     return mq, vq, ms, vs
+
+
+def random_fp8_codes(shape, seed: int, *, signed: bool, device="cpu"):
+    """Uniform random E4M3 codes (float8_e4m3fn) over the finite values: magnitude bytes
+    0x00-0x7E (0x7F is NaN), with a random sign when ``signed``."""
+    g = torch.Generator(device=device)
+    g.manual_seed(int(seed))
+    b = torch.randint(0, 0x7F, tuple(shape), generator=g, device=device, dtype=torch.int32)
+    if signed:
+        b |= torch.randint(0, 2, tuple(shape), generator=g, device=device, dtype=torch.int32) << 7
+    return b.to(torch.uint8).view(torch.float8_e4m3fn)
+
+
+def random_fp8_state(mat: Matrix, wl: Workload, device="cpu"):
+    """Random fp8 state for timing: E4M3 codes of W (fp8 weights) and of m and sqrt(v) (fp8
+    moments), each with an amax ring of 4 float32 slots filled with 3 standard deviations
+    of the tensor's warm magnitude (w_std, m_std, sqrt(v_std)).  Returns (W, w_ring, m,
+    m_ring, v, v_ring); the entries of the parts in bf16 are None."""
+    shape = (mat.d_out, mat.d_in)
+    ring = lambda a: torch.full((4,), float(a), device=device, dtype=torch.float32)
+    W = w_ring = m = m_ring = v = v_ring = None
+    if wl.weight == "fp8":
+        W = random_fp8_codes(shape, seed_of(mat.base, 7), signed=True, device=device)
+        w_ring = ring(3 * wl.w_std)
+    if wl.moment == "fp8":
+        m = random_fp8_codes(shape, seed_of(mat.base, 8), signed=True, device=device)
+        v = random_fp8_codes(shape, seed_of(mat.base, 9), signed=False, device=device)
+        m_ring, v_ring = ring(3 * wl.m_std), ring(3 * wl.v_std ** 0.5)
+    return W, w_ring, m, m_ring, v, v_ring
 
 
 def bf16_bits(t: torch.Tensor):
