@@ -7,11 +7,11 @@
 //                that the token axis, the GEMM's K, is contiguous), and accumulate
 //                G_tile = dY_tile^T X_tile with v_mfma_f32_32x32x16_bf16 into fp32
 //                registers; at the end they drop the accumulator tile into LDS.
-//   stream waves issue every global load of the tile's W, m, v (and int8 scales) when
-//                the workgroup starts, so that this HBM traffic overlaps the mainloop
-//                (vmcnt is per wave, so the math waves never wait on it); then they run
-//                the AdamW epilogue on the LDS copy of G with coalesced 16-byte accesses
-//                and store W, m, v.  G never leaves the chip.
+//   stream waves issue the global loads of the tile's W, m, v (and int8 scales) early in
+//                the mainloop, right after the DMA of its first chunks, so that this HBM
+//                traffic overlaps the mainloop (vmcnt is per wave, so the math waves never
+//                wait on it); then they run the AdamW epilogue on the LDS copy of G with
+//                coalesced 16-byte accesses and store W, m, v.  G never leaves the chip.
 //
 // The two-kernel comparison path reuses the same pieces: the store-G GEMM runs the same
 // mainloop with an epilogue that writes G, and the stand-alone optimizer stages a tile
