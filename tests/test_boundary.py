@@ -165,6 +165,37 @@ def test_paper_bytes_per_parameter():
     assert g["standard_bf16"] / g["fused_bf16"] == pytest.approx(g["memory_bound_speedup_bound"], abs=0.005)  # printed to 2 decimals
 
 
+def test_encoding_bytes_per_parameter():
+    """The state each encoding moves per parameter, read once and written once: W (bf16 2 B,
+    fp8 1 B) and the two moments (bf16 2 B, 8-bit 1 B), plus X and dY once per matrix and
+    the int8 scales; fp8 rings are per tensor and not counted."""
+    T, d_out, d_in = 512, 4096, 14336
+    P = d_out * d_in
+    xy = 2 * T * (d_in + d_out)
+    assert accounting.fused_bytes(T, d_in, d_out, "fp8") == 8 * P + xy
+    assert accounting.fused_bytes(T, d_in, d_out, "bf16", "fp8") == 10 * P + xy
+    assert accounting.fused_bytes(T, d_in, d_out, "fp8", "fp8") == 6 * P + xy
+    assert accounting.fused_bytes(T, d_in, d_out, "i8") == 8 * P + xy + 16 * (d_out // 256) * d_in
+    assert accounting.fused_bytes(T, d_in, d_out, "i8r64") == 8 * P + xy + 16 * d_out * (d_in // 64)
+
+
+def test_random_fp8_state_is_finite_e4m3_with_rings():
+    import torch
+    from paper_2606_22932_amd import synth
+    wl = synth.WORKLOADS["mlp_wfp8_fp8"]
+    mat = synth.Matrix("t", 96, 160, 3)
+    W, w_ring, m, m_ring, v, v_ring = synth.random_fp8_state(mat, wl)
+    for t in (W, m, v):
+        assert t.dtype == torch.float8_e4m3fn and tuple(t.shape) == (96, 160)
+        assert torch.isfinite(t.float()).all()            # no 0x7F / 0xFF (NaN) codes
+    assert (v.view(torch.uint8) < 0x80).all()              # sqrt(v) codes are non-negative
+    assert (m.view(torch.uint8) >= 0x80).any() and (W.view(torch.uint8) >= 0x80).any()
+    for r, a in ((w_ring, 3 * wl.w_std), (m_ring, 3 * wl.m_std), (v_ring, 3 * wl.v_std ** 0.5)):
+        assert r.dtype == torch.float32 and r.numel() == 4 and torch.allclose(r, torch.full((4,), a))
+    none = synth.random_fp8_state(mat, synth.WORKLOADS["mlp"])
+    assert all(t is None for t in none)
+
+
 # ----------------------------------------------------------------------------- grouped step
 
 def _mat(i, d_in=128, d_out=256, **over):
