@@ -3,7 +3,8 @@ scales), fp8 weights, and both, against the oracle.
 
 Shapes: ragged and multi-tile ones, the smallest legal shape, and the full Llama-3.1-8B
 o_proj shape (T=512, 4096 x 4096), where the per-tensor amax is a maximum over the records
-of 4096 waves.  Three consecutive steps from a cold start exercise the whole amax ring
+of 4096 waves, and the MLP down projection (4096 x 14336, 14336 waves), the shape bench.py
+times the fp8 encodings on.  Three consecutive steps from a cold start exercise the whole amax ring
 (decode with slot (t-2)%4, encode with (t-1)%4, record into t%4, clear (t+1)%4).  Each step
 the oracle starts from the GPU's own state (teacher forcing), so that a rounding tie decided
 differently in one step does not compound.
@@ -85,7 +86,8 @@ def check_ring(gpu, ora, slot, name):
 MODES = {"m": (False, True), "w": (True, False), "wm": (True, True)}
 
 
-@pytest.mark.parametrize("shape", [(77, 328, 200), (256, 264, 520), (1, 8, 8), (512, 4096, 4096)],
+@pytest.mark.parametrize("shape", [(77, 328, 200), (256, 264, 520), (1, 8, 8), (512, 4096, 4096),
+                                   (512, 14336, 4096)],
                          ids=lambda s: "x".join(map(str, s)))
 @pytest.mark.parametrize("mode", list(MODES))
 def test_fp8_three_steps_from_cold_start(mode, shape):

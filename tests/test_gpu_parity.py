@@ -99,6 +99,9 @@ def _full_matrix(wl_name, idx, step=100):
     p = Problem(bits(X), bits(dY), bits(W), None, None, wl.moment, hp=dict(wl.hyper))
     if wl.moment == "bf16":
         p.m, p.v = bits(m.to(torch.bfloat16)), bits(v.to(torch.bfloat16))
+    elif wl.moment == "i8r64":
+        p.m, p.m_scale = oracle.quantize_i8_row64(m.double().numpy(), second_moment=False)
+        p.v, p.v_scale = oracle.quantize_i8_row64(v.double().numpy(), second_moment=True)
     else:
         p.m, p.m_scale = oracle.quantize_i8(m.double().numpy(), False)
         p.v, p.v_scale = oracle.quantize_i8(v.double().numpy(), True)
@@ -125,6 +128,13 @@ def test_mlp_bf16_full(idx):
 @pytest.mark.parametrize("idx", [0, 1, 2], ids=["gate", "up", "down"])
 def test_mlp_int8_full(idx):
     _full_matrix("mlp_i8", idx)
+
+
+@pytest.mark.parametrize("idx", [0, 1, 2], ids=["gate", "up", "down"])
+def test_mlp_int8_rows_full(idx):
+    """The paper's own int8 layout (one scale per 64 elements of a row) on every element of
+    the MLP projections, the shapes bench.py times it on."""
+    _full_matrix("mlp_i8r64", idx)
 
 
 @pytest.mark.parametrize("moment", ["f32", "bf16", "i8", "i8r64"])
