@@ -32,56 +32,70 @@ COPY_BYTES = 1 << 30           # size of the calibration copy (--copy-calibratio
 # --no-unfused --copy-calibration` (FETCH_SIZE, then WRITE_SIZE), each counter scaled by
 # COPY_BYTES / (what it reads for the calibration copy).  Valid only for the kernel
 # sources whose sha256 is recorded: after any change to them the figure is reported as null.
-# (The counters below were taken on sources whose only difference from the recorded ones is
-# a comment; the device assembly of the two is identical but for the compilation-unit id.)
 TRAFFIC = {
     "sweep": {
-        "source_sha256": "80089c38cefc22d4d9cc72330cb7e132845f95967f752bede858e7faf02245f3",
-        "fetch_kib_per_launch": 209017.3,     # FETCH_SIZE, mean over the 129 launches of a step
-        "write_kib_per_launch": 340883.2,     # WRITE_SIZE
+        "source_sha256": "677b4262d806e9f2487b6194ae2608a6f74bb4e24408d3cec30f82f4d917b53d",
+        "fetch_kib_per_launch": 208083.6,     # FETCH_SIZE, mean over the 129 launches of a step
+        "write_kib_per_launch": 340903.9,     # WRITE_SIZE
         "fetch_scale": 1.99992,               # 1 GiB copy: FETCH_SIZE reads about 524300 KiB
         "write_scale": 1.0,                   # 1 GiB copy: WRITE_SIZE reads 1048576 KiB
-        "bytes_per_launch": 777115590,        # (fetch * fetch_scale + write * write_scale) KiB
+        "bytes_per_launch": 775223790,        # (fetch * fetch_scale + write * write_scale) KiB
     },
-    "mlp_i8": {
-        "source_sha256": "80089c38cefc22d4d9cc72330cb7e132845f95967f752bede858e7faf02245f3",
-        "fetch_kib_per_launch": 152790.6,     # mean over the 3 launches (gate, up, down)
-        "write_kib_per_launch": 262457.9,
-        "fetch_scale": 1.99989,
-        "write_scale": 1.0,
-        "bytes_per_launch": 581655497,
-    },
-    "mlp_i8r64": {
-        "source_sha256": "80089c38cefc22d4d9cc72330cb7e132845f95967f752bede858e7faf02245f3",
-        "fetch_kib_per_launch": 155854.9,     # mean over the 3 launches (gate, up, down)
-        "write_kib_per_launch": 240778.8,
-        "fetch_scale": 1.99992,
-        "write_scale": 1.0,
-        "bytes_per_launch": 565736070,
-    },
-    "mlp_fp8": {
-        "source_sha256": "80089c38cefc22d4d9cc72330cb7e132845f95967f752bede858e7faf02245f3",
-        "fetch_kib_per_launch": 147132.5,     # mean over the 3 launches (gate, up, down)
-        "write_kib_per_launch": 229395.3,
+    "o_proj": {
+        "source_sha256": "677b4262d806e9f2487b6194ae2608a6f74bb4e24408d3cec30f82f4d917b53d",
+        "fetch_kib_per_launch": 61657.5,     # one launch (4096 x 4096)
+        "write_kib_per_launch": 98401.0,
         "fetch_scale": 1.99993,
         "write_scale": 1.0,
-        "bytes_per_launch": 536216860,
+        "bytes_per_launch": 227032473,
+    },
+    "mlp": {
+        "source_sha256": "677b4262d806e9f2487b6194ae2608a6f74bb4e24408d3cec30f82f4d917b53d",
+        "fetch_kib_per_launch": 211172.7,     # mean over the 3 launches (gate, up, down)
+        "write_kib_per_launch": 344073.3,
+        "fetch_scale": 1.99993,
+        "write_scale": 1.0,
+        "bytes_per_launch": 784796715,
+    },
+    "mlp_i8": {
+        "source_sha256": "677b4262d806e9f2487b6194ae2608a6f74bb4e24408d3cec30f82f4d917b53d",
+        "fetch_kib_per_launch": 153124.5,     # mean over the 3 launches (gate, up, down)
+        "write_kib_per_launch": 261589.0,
+        "fetch_scale": 1.99992,
+        "write_scale": 1.0,
+        "bytes_per_launch": 581454198,
+    },
+    "mlp_i8r64": {
+        "source_sha256": "677b4262d806e9f2487b6194ae2608a6f74bb4e24408d3cec30f82f4d917b53d",
+        "fetch_kib_per_launch": 155839.9,     # mean over the 3 launches (gate, up, down)
+        "write_kib_per_launch": 241004.1,
+        "fetch_scale": 1.99993,
+        "write_scale": 1.0,
+        "bytes_per_launch": 565936401,
+    },
+    "mlp_fp8": {
+        "source_sha256": "677b4262d806e9f2487b6194ae2608a6f74bb4e24408d3cec30f82f4d917b53d",
+        "fetch_kib_per_launch": 147209.0,     # mean over the 3 launches (gate, up, down)
+        "write_kib_per_launch": 229400.2,
+        "fetch_scale": 1.99992,
+        "write_scale": 1.0,
+        "bytes_per_launch": 536378457,
     },
     "mlp_wfp8": {
-        "source_sha256": "80089c38cefc22d4d9cc72330cb7e132845f95967f752bede858e7faf02245f3",
-        "fetch_kib_per_launch": 178042.5,     # mean over the 3 launches (gate, up, down)
-        "write_kib_per_launch": 286730.1,
+        "source_sha256": "677b4262d806e9f2487b6194ae2608a6f74bb4e24408d3cec30f82f4d917b53d",
+        "fetch_kib_per_launch": 177867.1,     # mean over the 3 launches (gate, up, down)
+        "write_kib_per_launch": 286732.6,
         "fetch_scale": 1.99992,
         "write_scale": 1.0,
-        "bytes_per_launch": 658228770,
+        "bytes_per_launch": 657871851,
     },
     "mlp_wfp8_fp8": {
-        "source_sha256": "80089c38cefc22d4d9cc72330cb7e132845f95967f752bede858e7faf02245f3",
-        "fetch_kib_per_launch": 116025.8,     # mean over the 3 launches (gate, up, down)
-        "write_kib_per_launch": 172061.6,
+        "source_sha256": "677b4262d806e9f2487b6194ae2608a6f74bb4e24408d3cec30f82f4d917b53d",
+        "fetch_kib_per_launch": 116193.0,     # mean over the 3 launches (gate, up, down)
+        "write_kib_per_launch": 172065.1,
         "fetch_scale": 1.99992,
         "write_scale": 1.0,
-        "bytes_per_launch": 413802564,
+        "bytes_per_launch": 414148815,
     },
 }
 
