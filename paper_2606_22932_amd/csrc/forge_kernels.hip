@@ -466,8 +466,10 @@ template <> struct Rule<EPI_MUON> {           // B' = mu B + G (the GEMM's beta)
 };
 
 // The epilogue of a rule on fp32 or bf16 state.  The stream waves prefetch the tile's
-// bf16 W and state into registers while the mainloop runs (fp32 state would not fit and
-// is loaded here); then each lane updates 8 consecutive columns of one row per pass.
+// W and state into registers while the mainloop runs (bf16 state: six or eight of the
+// eight row passes; fp32 state, twice the bytes: four), then each lane updates 8
+// consecutive columns of one row per pass, loading later passes' state a fixed number of
+// passes ahead.
 // Byte offset of element (p, q) of a [rows, ld] tensor with `eb`-byte elements, or an
 // offset past every buffer end (reads zero) when the element lies outside the tensor.
 __device__ __forceinline__ uint32_t elem_off(int p, int q, int rows, int ld, int eb)
@@ -487,32 +489,56 @@ template <int BP, int BQ, int MK, int E, int AH = 0>
 struct EpiRule {
     using M = EpiMap<BP, BQ>;
     using R = Rule<E>;
-    static constexpr bool PREFETCH = (MK == MK_BF16);
-    static constexpr int NPF = PREFETCH ? M::NPASS : 1;
-    // Row passes whose state is loaded while the mainloop runs (AH, or by default all but
-    // two); the loads of the others are issued as the epilogue starts, AHEAD passes before
-    // their use.  Less state in flight per CU suits in-place HBM traffic, fewer than six
-    // passes loses overlap with the GEMM; the launcher picks all eight for long launches.
+    static_assert(MK == MK_BF16 || MK == MK_F32, "the rule epilogue keeps bf16 or fp32 state");
+    static constexpr bool F32 = (MK == MK_F32);
+    static constexpr int NPF = M::NPASS;
+    // Row passes whose state is loaded while the mainloop runs (bf16 state: AH, or by
+    // default all but two); the loads of the others are issued as the epilogue starts,
+    // AHEAD passes before their use.  Less state in flight per CU suits in-place HBM
+    // traffic, fewer than six passes loses overlap with the GEMM; the launcher picks all
+    // eight for long launches.  fp32 state: four passes, 80 B per lane each with the bf16 W
+    // (at most 128 VGPRs; on the 4096 x 4096 microbenchmark AdamW took 99.5-99.8 against
+    // 106 us at T = 512 and SGD with momentum 58.7-58.9 against 65.5 us, with no prefetch).
 #ifdef FORGE_PF_AHEAD
     static constexpr int AHEAD = FORGE_PF_AHEAD < M::NPASS ? FORGE_PF_AHEAD : M::NPASS;
 #else
-    static constexpr int AHEAD = AH > 0 ? (AH < M::NPASS ? AH : M::NPASS) : (M::NPASS > 2 ? M::NPASS - 2 : M::NPASS);
+    static constexpr int AHEAD = F32 ? 4
+                               : AH > 0 ? (AH < M::NPASS ? AH : M::NPASS) : (M::NPASS > 2 ? M::NPASS - 2 : M::NPASS);
 #endif
-    u32x4_t pw[R::W_RW ? NPF : 1], ps1[R::NS >= 1 ? NPF : 1], ps2[R::NS >= 2 ? NPF : 1];
+    // packed bf16 state: one 16-byte word per pass and lane; fp32 state: two
+    static constexpr int SW = F32 ? 2 : 1;
+    u32x4_t pw[R::W_RW ? NPF : 1], ps1[R::NS >= 1 ? NPF : 1][SW], ps2[R::NS >= 2 ? NPF : 1][SW];
 
     // Loads of pass I (one row per lane) into the prefetch registers.
     template <int I>
     __device__ __forceinline__ void prefetch_pass(const Args &a, int p0, int q0, int s)
     {
-        if constexpr (PREFETCH) {
-            // buffer loads: elements outside the matrix read as zero
-            const int rs = s / M::LPR, q = q0 + (s % M::LPR) * 8;
-            const int p = p0 + I * M::RPP + rs;
-            const uint64_t n = 2ull * (uint64_t)a.d_out * (uint64_t)a.d_in;
-            const uint32_t off = elem_off(p, q, a.d_out, a.d_in, 2);
-            if constexpr (R::W_RW) pw[I] = __builtin_amdgcn_raw_buffer_load_b128(rsrc_of(a.W, n), off, 0, 2);
-            if constexpr (R::NS >= 1) ps1[I] = __builtin_amdgcn_raw_buffer_load_b128(rsrc_of(a.m, n), off, 0, 2);
-            if constexpr (R::NS >= 2) ps2[I] = __builtin_amdgcn_raw_buffer_load_b128(rsrc_of(a.v, n), off, 0, 2);
+        // buffer loads: elements outside the matrix read as zero
+        const int rs = s / M::LPR, q = q0 + (s % M::LPR) * 8;
+        const int p = p0 + I * M::RPP + rs;
+        const uint64_t n = 2ull * (uint64_t)a.d_out * (uint64_t)a.d_in;
+        const uint32_t off = elem_off(p, q, a.d_out, a.d_in, 2);
+        if constexpr (R::W_RW) pw[I] = __builtin_amdgcn_raw_buffer_load_b128(rsrc_of(a.W, n), off, 0, 2);
+        if constexpr (!F32) {
+            if constexpr (R::NS >= 1) ps1[I][0] = __builtin_amdgcn_raw_buffer_load_b128(rsrc_of(a.m, n), off, 0, 2);
+            if constexpr (R::NS >= 2) ps2[I][0] = __builtin_amdgcn_raw_buffer_load_b128(rsrc_of(a.v, n), off, 0, 2);
+        } else {
+            // an fp32 tensor may pass 4 GB, beyond a buffer's 32-bit offsets: loads
+            // masked to the matrix, zero outside it
+            const bool ok = p < a.d_out && q < a.d_in;
+            const size_t e = (size_t)p * a.d_in + q;
+#pragma unroll
+            for (int k = 0; k < 2; ++k) {
+                if constexpr (R::NS >= 1) ps1[I][k] = u32x4_t{0u, 0u, 0u, 0u};
+                if constexpr (R::NS >= 2) ps2[I][k] = u32x4_t{0u, 0u, 0u, 0u};
+            }
+            if (ok) {
+#pragma unroll
+                for (int k = 0; k < 2; ++k) {
+                    if constexpr (R::NS >= 1) ps1[I][k] = ld_nt<u32x4_t>(static_cast<const float *>(a.m) + e + 4 * k);
+                    if constexpr (R::NS >= 2) ps2[I][k] = ld_nt<u32x4_t>(static_cast<const float *>(a.v) + e + 4 * k);
+                }
+            }
         }
     }
 
@@ -541,18 +567,6 @@ struct EpiRule {
         return e < 4 ? x0[e] : x1[e - 4];
     }
 
-    static __device__ __forceinline__ void load_f32(const void *base, size_t off, bool ok, f32x4_t &x0,
-                                                    f32x4_t &x1)
-    {
-        x0 = f32x4_t{0, 0, 0, 0};
-        x1 = x0;
-        if (ok) {
-            const float *p = static_cast<const float *>(base) + off;
-            x0 = ld_nt<f32x4_t>(p);
-            x1 = ld_nt<f32x4_t>(p + 4);
-        }
-    }
-
     static __device__ __forceinline__ void store_state(void *base, size_t off, const float (&f)[8])
     {
         if constexpr (MK == MK_BF16) {
@@ -573,8 +587,7 @@ struct EpiRule {
         const Hyper h = a.h;
 #pragma unroll
         for (int i = 0; i < M::NPASS; ++i) {
-            if constexpr (PREFETCH)
-                if (i + AHEAD < M::NPASS) prefetch_at(i + AHEAD, a, p0, q0, s);
+            if (i + AHEAD < M::NPASS) prefetch_at(i + AHEAD, a, p0, q0, s);
             const int p = p0 + i * M::RPP + rs;
             const bool ok = q < a.d_in && p < a.d_out;
             const size_t off = (size_t)p * a.d_in + q;
@@ -584,23 +597,28 @@ struct EpiRule {
             // W and the states stay packed until each element is needed
             u32x4_t w4 = {0u, 0u, 0u, 0u}, a4 = w4, b4 = w4;
             f32x4_t a0 = {0, 0, 0, 0}, a1 = a0, b0 = a0, b1 = a0;
-            if constexpr (PREFETCH) {
+            if constexpr (F32) {
                 if constexpr (R::W_RW) w4 = pw[i];
-                if constexpr (R::NS >= 1) a4 = ps1[i];
-                if constexpr (R::NS >= 2) b4 = ps2[i];
+                if constexpr (R::NS >= 1) {
+                    a0 = __builtin_bit_cast(f32x4_t, ps1[i][0]);
+                    a1 = __builtin_bit_cast(f32x4_t, ps1[i][1]);
+                }
+                if constexpr (R::NS >= 2) {
+                    b0 = __builtin_bit_cast(f32x4_t, ps2[i][0]);
+                    b1 = __builtin_bit_cast(f32x4_t, ps2[i][1]);
+                }
             } else {
-                if constexpr (R::W_RW)
-                    if (ok) w4 = ld_nt<u32x4_t>(a.W + off);
-                if constexpr (R::NS >= 1) load_f32(a.m, off, ok, a0, a1);
-                if constexpr (R::NS >= 2) load_f32(a.v, off, ok, b0, b1);
+                if constexpr (R::W_RW) w4 = pw[i];
+                if constexpr (R::NS >= 1) a4 = ps1[i][0];
+                if constexpr (R::NS >= 2) b4 = ps2[i][0];
             }
             float wo[8], o1[8], o2[8];
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const float g = elt(g0, g1, e);
                 const float w = R::W_RW ? elt(w4, e) : 0.0f;
-                const float x = R::NS >= 1 ? (PREFETCH ? elt(a4, e) : elt(a0, a1, e)) : 0.0f;
-                const float y = R::NS >= 2 ? (PREFETCH ? elt(b4, e) : elt(b0, b1, e)) : 0.0f;
+                const float x = R::NS >= 1 ? (F32 ? elt(a0, a1, e) : elt(a4, e)) : 0.0f;
+                const float y = R::NS >= 2 ? (F32 ? elt(b0, b1, e) : elt(b4, e)) : 0.0f;
                 R::elem(g, w, x, y, h, wo[e], o1[e], o2[e]);
             }
             if (ok) {

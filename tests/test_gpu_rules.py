@@ -93,12 +93,15 @@ def test_rule_matches_oracle(name, shape, kind):
     _say(run_rule(name, *shape, kind, step=100))
 
 
+@pytest.mark.parametrize("kind", ["bf16", "f32"])
 @pytest.mark.parametrize("name", list(RULES))
-def test_rule_full_size_o_proj(name):
-    """Every element of the Llama-3.1-8B o_proj shape (T=512, 4096 x 4096, bf16 state): the
-    full tile grid of the single-layer configuration, not only a few tiles."""
-    _say(f"{name} full size 512x4096x4096 bf16")
-    _say(run_rule(name, 512, 4096, 4096, "bf16", step=100, seed=302))
+def test_rule_full_size_o_proj(name, kind):
+    """Every element of the Llama-3.1-8B o_proj shape (T=512, 4096 x 4096, bf16 or fp32
+    state): the full tile grid of the single-layer configuration, not only a few tiles, and
+    for fp32 state every pass of the prefetch (four passes loaded during the mainloop, the
+    rest four passes ahead in the epilogue)."""
+    _say(f"{name} full size 512x4096x4096 {kind}")
+    _say(run_rule(name, 512, 4096, 4096, kind, step=100, seed=302))
 
 
 @pytest.mark.parametrize("name", ["adagrad", "nadam", "radam", "adamax"])
