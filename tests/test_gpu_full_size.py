@@ -9,7 +9,8 @@ full problem has there, and a full-size GPU result can be checked on a sample.
   benchmark times it: ``forge_linear_step_grouped`` per backward-order group of matrices
   (``synth.launch_groups``), back to back on one stream.
 * The largest legal operands: X or dY with just under 2^31 elements and a ragged token
-  count, so the last token chunk runs past T at byte offsets beyond 2^32.
+  count, so the last token chunk runs past T at byte offsets beyond 2^32; and fp32 moments
+  of 1.56 G elements (6.2 GB each), whose rows lie beyond the 4 GB a buffer offset reaches.
 """
 import numpy as np
 import pytest
@@ -71,11 +72,12 @@ def test_sweep_sampled_rows_in_bench_configuration():
 # (T, d_in, d_out): X (then dY) with just under 2^31 elements, T ragged against the
 # 32-token chunk; chunk 1 holds one token row and its other rows lie past 2^32 bytes.
 D_MAX = 65075256          # 33 * D_MAX = 2147483448 < 2^31 - 1, and a multiple of 8
-MAX_SHAPES = [(33, D_MAX, 8, "bf16"), (33, D_MAX, 8, "i8"), (33, D_MAX, 8, "i8r64"), (33, 8, D_MAX, "bf16")]
+MAX_SHAPES = [(33, D_MAX, 8, "bf16"), (33, D_MAX, 8, "i8"), (33, D_MAX, 8, "i8r64"), (33, 8, D_MAX, "bf16"),
+              (33, D_MAX, 24, "f32")]
 
 
 @pytest.mark.parametrize("T,d_in,d_out,moment", MAX_SHAPES,
-                         ids=["X-2^31-bf16", "X-2^31-i8", "X-2^31-i8r64", "dY-2^31-bf16"])
+                         ids=["X-2^31-bf16", "X-2^31-i8", "X-2^31-i8r64", "dY-2^31-bf16", "X-2^31-f32-6GB-moments"])
 def test_maximum_operand_size(T, d_in, d_out, moment):
     _say(f"max size T={T} d_in={d_in} d_out={d_out} {moment}")
     device = torch.device("cuda:0")
@@ -89,7 +91,8 @@ def test_maximum_operand_size(T, d_in, d_out, moment):
     if moment in ("i8", "i8r64"):
         m, v, ms, vs = synth.random_i8_state(mat, wl, device=device, layout="col256" if moment == "i8" else "row64")
     else:
-        m, v = synth.warm_moments(mat, wl, device=device, dtype=torch.bfloat16)
+        m, v = synth.warm_moments(mat, wl, device=device,
+                                  dtype=torch.float32 if moment == "f32" else torch.bfloat16)
         ms = vs = None
     rng = np.random.default_rng(33)
     if moment == "i8r64":
