@@ -527,3 +527,34 @@ def test_library_has_no_undefined_internal_symbols():
         pytest.skip("nm not available")
     out = subprocess.run([nm, "-D", "--undefined-only", build.LIB], capture_output=True, text=True, check=True).stdout
     assert "forge_impl" not in out, out
+
+
+def test_missing_library_fails_loudly():
+    """Without the built HIP library every entry point raises: there is no CPU or PyTorch
+    fallback.  Run in a child process so that this process keeps its loaded library."""
+    import subprocess
+    import sys
+    code = (
+        "import torch\n"
+        "from paper_2606_22932_amd import build, forge\n"
+        "build.LIB = '/nonexistent/libforge.so'\n"
+        "for f in (forge.lib, lambda: forge.forge_status_string(0),\n"
+        "          lambda: forge.forge_query_tile(512, 4096, 4096, 1)):\n"
+        "    try:\n"
+        "        f()\n"
+        "    except RuntimeError as e:\n"
+        "        assert 'not built' in str(e) and 'no non-HIP fallback' in str(e), e\n"
+        "    else:\n"
+        "        raise SystemExit('an entry point ran without the library')\n"
+        "x, w = torch.zeros(4, 8, dtype=torch.bfloat16), torch.zeros(8, 8, dtype=torch.bfloat16)\n"
+        "try:\n"
+        "    forge.forge_linear_step(x, x, w, w.clone(), w.clone(), lr=1e-3, beta1=0.9, beta2=0.999,\n"
+        "                            eps=1e-8, weight_decay=0.0, step=1)\n"
+        "except Exception as e:\n"
+        "    print('step raised', type(e).__name__)\n"
+        "else:\n"
+        "    raise SystemExit('the step ran on host tensors without the library')\n"
+        "print('raised')\n")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    res = subprocess.run([sys.executable, "-c", code], cwd=root, capture_output=True, text=True, timeout=300)
+    assert res.returncode == 0 and "raised" in res.stdout, res.stdout + res.stderr
