@@ -32,11 +32,12 @@ COPY_BYTES = 1 << 30           # size of the calibration copy (--copy-calibratio
 # --no-unfused --copy-calibration` (FETCH_SIZE, then WRITE_SIZE), each counter scaled by
 # COPY_BYTES / (what it reads for the calibration copy).  Valid only for the kernel
 # sources whose sha256 is recorded: after any change to them the figure is reported as null.
-# (The counters were taken on sources with sha256 677b4262...; the edit since then changed
-# only the kernels of fp32 state, and every kernel below compiles to the same device code.)
+# (The counters were taken on sources with sha256 677b4262...; the edits since then changed
+# only the kernels of fp32 state and the host-side choice of prefetch depth for T >= 1024,
+# and every kernel below compiles to the same device code.)
 TRAFFIC = {
     "sweep": {
-        "source_sha256": "63ccc85a57fa82b91d39cb8d2d6a2af81ba3a6c87853d2e66e8d883dc1efbb53",
+        "source_sha256": "54af42890281bf2601782e57ddc2958da3fb445485e524a10dc786cc63449554",
         "fetch_kib_per_launch": 208083.6,     # FETCH_SIZE, mean over the 129 launches of a step
         "write_kib_per_launch": 340903.9,     # WRITE_SIZE
         "fetch_scale": 1.99992,               # 1 GiB copy: FETCH_SIZE reads about 524300 KiB
@@ -44,7 +45,7 @@ TRAFFIC = {
         "bytes_per_launch": 775223790,        # (fetch * fetch_scale + write * write_scale) KiB
     },
     "o_proj": {
-        "source_sha256": "63ccc85a57fa82b91d39cb8d2d6a2af81ba3a6c87853d2e66e8d883dc1efbb53",
+        "source_sha256": "54af42890281bf2601782e57ddc2958da3fb445485e524a10dc786cc63449554",
         "fetch_kib_per_launch": 61657.5,     # one launch (4096 x 4096)
         "write_kib_per_launch": 98401.0,
         "fetch_scale": 1.99993,
@@ -52,7 +53,7 @@ TRAFFIC = {
         "bytes_per_launch": 227032473,
     },
     "mlp": {
-        "source_sha256": "63ccc85a57fa82b91d39cb8d2d6a2af81ba3a6c87853d2e66e8d883dc1efbb53",
+        "source_sha256": "54af42890281bf2601782e57ddc2958da3fb445485e524a10dc786cc63449554",
         "fetch_kib_per_launch": 211172.7,     # mean over the 3 launches (gate, up, down)
         "write_kib_per_launch": 344073.3,
         "fetch_scale": 1.99993,
@@ -60,7 +61,7 @@ TRAFFIC = {
         "bytes_per_launch": 784796715,
     },
     "mlp_i8": {
-        "source_sha256": "63ccc85a57fa82b91d39cb8d2d6a2af81ba3a6c87853d2e66e8d883dc1efbb53",
+        "source_sha256": "54af42890281bf2601782e57ddc2958da3fb445485e524a10dc786cc63449554",
         "fetch_kib_per_launch": 153124.5,     # mean over the 3 launches (gate, up, down)
         "write_kib_per_launch": 261589.0,
         "fetch_scale": 1.99992,
@@ -68,7 +69,7 @@ TRAFFIC = {
         "bytes_per_launch": 581454198,
     },
     "mlp_i8r64": {
-        "source_sha256": "63ccc85a57fa82b91d39cb8d2d6a2af81ba3a6c87853d2e66e8d883dc1efbb53",
+        "source_sha256": "54af42890281bf2601782e57ddc2958da3fb445485e524a10dc786cc63449554",
         "fetch_kib_per_launch": 155839.9,     # mean over the 3 launches (gate, up, down)
         "write_kib_per_launch": 241004.1,
         "fetch_scale": 1.99993,
@@ -76,7 +77,7 @@ TRAFFIC = {
         "bytes_per_launch": 565936401,
     },
     "mlp_fp8": {
-        "source_sha256": "63ccc85a57fa82b91d39cb8d2d6a2af81ba3a6c87853d2e66e8d883dc1efbb53",
+        "source_sha256": "54af42890281bf2601782e57ddc2958da3fb445485e524a10dc786cc63449554",
         "fetch_kib_per_launch": 147209.0,     # mean over the 3 launches (gate, up, down)
         "write_kib_per_launch": 229400.2,
         "fetch_scale": 1.99992,
@@ -84,7 +85,7 @@ TRAFFIC = {
         "bytes_per_launch": 536378457,
     },
     "mlp_wfp8": {
-        "source_sha256": "63ccc85a57fa82b91d39cb8d2d6a2af81ba3a6c87853d2e66e8d883dc1efbb53",
+        "source_sha256": "54af42890281bf2601782e57ddc2958da3fb445485e524a10dc786cc63449554",
         "fetch_kib_per_launch": 177867.1,     # mean over the 3 launches (gate, up, down)
         "write_kib_per_launch": 286732.6,
         "fetch_scale": 1.99992,
@@ -92,7 +93,7 @@ TRAFFIC = {
         "bytes_per_launch": 657871851,
     },
     "mlp_wfp8_fp8": {
-        "source_sha256": "63ccc85a57fa82b91d39cb8d2d6a2af81ba3a6c87853d2e66e8d883dc1efbb53",
+        "source_sha256": "54af42890281bf2601782e57ddc2958da3fb445485e524a10dc786cc63449554",
         "fetch_kib_per_launch": 116193.0,     # mean over the 3 launches (gate, up, down)
         "write_kib_per_launch": 172065.1,
         "fetch_scale": 1.99992,

@@ -1744,12 +1744,16 @@ static hipError_t launch_group(const Args *a, int n, hipStream_t st)
     }
     if (g.start[n] == 0) return hipSuccess;
     // Prefetch depth by launch length (AdamW on bf16 state): a launch of at least 8 waves of
-    // resident tiles loads all eight row passes of a tile's state during its mainloop, a
-    // shorter one six.  Measured per launch group of the Llama-3.1-8B sweep at T = 512:
-    // lm_head (63 waves) 1157 against 1222 us, gate+up (14) even, down (7), o (2) and
-    // q+k+v (3) 1-7 % slower with eight.
+    // resident tiles, or with a long token loop (T >= 1024 in every matrix), loads all eight
+    // row passes of a tile's state during its mainloop, a shorter one six.  Measured per
+    // launch group of the Llama-3.1-8B sweep at T = 512: lm_head (63 waves) 1157 against
+    // 1222 us, gate+up (14) even, down (7), o (2) and q+k+v (3) 1-7 % slower with eight; on
+    // 4096 x 4096 over three rotated copies, eight were 2-4.5 % faster at T = 1024-4096
+    // (T = 4096: 145.9-146.4 against 148.9-149.1 us).
+    int min_t = a[0].T;
+    for (int i = 1; i < n; ++i) min_t = a[i].T < min_t ? a[i].T : min_t;
     if constexpr (MK == MK_BF16 && EPI == EPI_ADAMW)
-        if (g.start[n] >= 8 * 2 * device_cu_count()) {
+        if (g.start[n] >= 8 * 2 * device_cu_count() || min_t >= 1024) {
             hipLaunchKernelGGL((fused_kernel<BP, BQ, MK, EPI, 8>), dim3(g.start[n]), dim3(NT), 0, st, g);
             return hipGetLastError();
         }

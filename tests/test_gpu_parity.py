@@ -276,7 +276,8 @@ def test_grouped_shared_input_and_empty_member():
 
 def test_long_launch_prefetch_depth_bitwise():
     """A launch of at least 8 waves of resident tiles (4096 tiles of 128x128 on 256 CUs)
-    prefetches all eight row passes of a tile's state, a shorter one six.  The depth changes
+    prefetches all eight row passes of a tile's state, a shorter one six (at T < 1024; from
+    T = 1024 every launch takes eight, which the T = 4096 tests cover).  The depth changes
     when loads are issued, not what is computed: four o_proj-sized matrices in one grouped
     launch (4096 tiles) give the bits of four single launches (1024 tiles each), and the
     first is checked against the oracle on every element."""
